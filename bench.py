@@ -1,0 +1,242 @@
+"""Benchmark of the Clifford convolution forward pass on one MI355X.
+
+One step = one pass of the workload's whole forward path over its batch:
+every convolution layer through the C ABI (clifford_conv_nd, automatic kernel
+choice) with the bias and, for the blocks, the multivector activation fused
+into the convolution; inputs and parameters already resident in HBM.
+
+Prints one JSON line.  ``value`` is useful GFLOP/s of the headline workload
+(2D, g=(1,1), B=8, C_in=C_out=64, d_image=128, d_filter=3), useful FLOPs =
+2 B C_out C_in N_B^2 d_filter^k d_out^k per convolution.  ``roofline`` is the
+dominant kernel's achieved TFLOP/s (useful FLOPs per launch / its average
+duration from HIP events on the launch stream) against the fp32 matrix-core
+peak.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the
+same workload on this host.  ``workloads`` reports the other workloads the
+same way (3D single conv; 2D/3D blocks with the fused-activation overhead).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+PEAK_FP32_MFMA_TFLOPS = 157.3   # 256 CU x 2.4 GHz x 256 FLOP/clk/CU
+PEAK_HBM_GBS = 8000.0
+HEADLINE = "c2_2d_c64_d128"
+KERNEL_SOURCES = ["paper_2507_01040_amd/csrc/conv_mfma.hip",
+                  "paper_2507_01040_amd/csrc/common.hpp",
+                  "paper_2507_01040_amd/csrc/epilogue.hpp"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+class Runner:
+    """Device-resident inputs and preallocated outputs of one workload."""
+
+    def __init__(self, w: W.Workload, fuse_act: bool = True):
+        import torch
+        import paper_2507_01040_amd as P
+        self.P, self.torch, self.w = P, torch, w
+        x, params = W.make_inputs(w)
+        self.host_x, self.host_params = x, params
+        dev = torch.device("cuda:0")
+        self.x = torch.from_numpy(x).to(dev)
+        self.layers = []
+        for p, act in zip(params, w.acts):
+            a = None
+            if act is not None and fuse_act:
+                a = (act.mode, act.blades,
+                     None if p.act_weight is None else torch.from_numpy(p.act_weight).to(dev),
+                     None if p.act_bias is None else torch.from_numpy(p.act_bias).to(dev))
+            self.layers.append((torch.from_numpy(p.filters).to(dev),
+                                torch.from_numpy(p.bias).to(dev), a))
+        self.outs = [torch.empty(s.output_shape(), dtype=torch.float32, device=dev)
+                     for s in w.layers]
+        self.g = w.layers[0].g
+
+    def step(self, events=None):
+        y = self.x
+        for li, (f, b, a) in enumerate(self.layers):
+            if events is not None:
+                events[li][0].record()
+            y = self.P.conv_nd(y, f, b, self.g, act=a, out=self.outs[li])
+            if events is not None:
+                events[li][1].record()
+        return y
+
+    def time(self, steps: int, warmup: int):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        n_l = len(self.layers)
+        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n_l)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            self.step([ev[s][l] for l in range(n_l)])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per_layer_ms = [float(np.mean([ev[s][l][0].elapsed_time(ev[s][l][1])
+                                       for s in range(steps)])) for l in range(n_l)]
+        return wall / steps * 1e3, per_layer_ms
+
+
+def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
+    """The fp64 oracle on a bounded sample: the first batch entries of the
+    workload (as many as fit the time budget, at least one)."""
+    import oracle
+    x, params = W.make_inputs(w)
+    threads = oracle.default_threads()
+    done_flops, t_total, nb_done = 0, 0.0, 0
+    for b in range(w.layers[0].B):
+        xb = x[b:b + 1]
+        t0 = time.perf_counter()
+        y = xb
+        for p, a, s in zip(params, w.acts, w.layers):
+            y = oracle.conv_nd(y, p.filters, p.bias, s.g, nthreads=threads)
+            if a is not None:
+                y = oracle.act(y, a.mode, a.blades, p.act_weight, p.act_bias)
+        t_total += time.perf_counter() - t0
+        done_flops += w.useful_flops // w.layers[0].B
+        nb_done += 1
+        if t_total >= budget_s:
+            break
+    return {"value": round(done_flops / t_total / 1e9, 3), "unit": "GFLOP/s",
+            "cores": threads, "kind": "oracle",
+            "sample": "%s, batch entries 0..%d of %d (%.2f useful GFLOP), fp64, %.1f s"
+                      % (w.name, nb_done - 1, w.layers[0].B, done_flops / 1e9, t_total)}
+
+
+def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False):
+    w = W.WORKLOADS[name]
+    r = Runner(w)
+    ms, per_layer = r.time(steps, warmup)
+    flops = w.useful_flops
+    res = {"workload": name, "ms_per_step": round(ms, 4),
+           "useful_gflops": round(flops / (ms * 1e-3) / 1e9, 1),
+           "kernel_ms": [round(v, 4) for v in per_layer],
+           "kernel_tflops": [round(l.useful_flops() / (t * 1e-3) / 1e12, 2)
+                             for l, t in zip(w.layers, per_layer)]}
+    res["frac_of_fp32_mfma_peak"] = round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
+    if epilogue_overhead and any(a is not None for a in w.acts):
+        plain = Runner(w, fuse_act=False)
+        ms_plain, per_plain = plain.time(steps, warmup)
+        res["bias_only_kernel_ms"] = [round(v, 4) for v in per_plain]
+        res["fused_act_overhead"] = round(sum(per_layer) / sum(per_plain) - 1.0, 4)
+        del plain
+    del r
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=HEADLINE, choices=W.WORKLOAD_ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the other workloads (profiling runs)")
+    ap.add_argument("--copy-calib", type=int, default=0,
+                    help="only run N copies of 1 GiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the convolution would shard over the batch with no exchange); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2507_01040_amd as P
+    P.load()
+    if args.copy_calib:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda:0").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(args.copy_calib):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calib_bytes": src.numel() * 4, "copies": args.copy_calib}))
+        return
+
+    w = W.WORKLOADS[args.workload]
+    head = measure(args.workload, args.steps, args.warmup,
+                   epilogue_overhead=not args.no_extra)
+    s0 = w.layers[0]
+    dom = int(np.argmax(head["kernel_ms"]))
+    dom_ms = head["kernel_ms"][dom]
+    achieved = w.layers[dom].useful_flops() / (dom_ms * 1e-3) / 1e12
+    line = {
+        "metric": "Clifford conv useful GFLOP/s (2D/3D) and % of fp32 MFMA peak on 1 MI355X",
+        "value": head["useful_gflops"],
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded numpy, shapes and distributions of the workload)",
+        "config": {"workload": args.workload, "k": s0.k, "g": list(s0.g), "B": s0.B,
+                   "C_in": s0.C_in, "C_out": s0.C_out, "d_image": s0.d_image,
+                   "d_filter": s0.d_filter, "layers": len(w.layers),
+                   "act": [None if a is None else {"mode": W.AGG_NAMES[a.mode],
+                                                   "blades": list(a.blades)}
+                           for a in w.acts]},
+        "frac_of_fp32_mfma_peak": head["frac_of_fp32_mfma_peak"],
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_FP32_MFMA_TFLOPS, 4),
+                     "traffic": _traffic(args.workload),
+                     "kernel": "conv_mfma_kernel (layer %d)" % dom,
+                     "kernel_ms": dom_ms,
+                     "kernel_source_hash": kernel_source_hash()},
+    }
+    if not args.no_extra:
+        extra = {}
+        for name in W.WORKLOAD_ORDER:
+            if name == args.workload:
+                continue
+            extra[name] = measure(name, max(3, min(args.steps, 10)), 2,
+                                  epilogue_overhead=True)
+            torch.cuda.empty_cache()
+        line["workloads"] = extra
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,165 @@
+/*
+ * cliffconv.h -- C ABI of the MI355X (gfx950) Clifford convolution library
+ * (libcliffconv.so).
+ *
+ * The operations are those of "Fast Clifford Neural Layers" (arXiv
+ * 2507.01040): the k-D Clifford convolution of Algorithm 1 with the bias add,
+ * and the multivector activation of Algorithm 3, usable on its own or fused
+ * as the convolution's epilogue.  All arithmetic is IEEE fp32 on the GPU.
+ *
+ * Algebra (paper, Background, "Clifford Algebra"): Cl_g(R^k) with signature
+ * g in {-1, 0, +1}^k, generators e_1..e_k, e_i e_i = g_i, e_i e_j = -e_j e_i.
+ * A signature is valid if at least one g_i is non-zero.  A multivector holds
+ * N_B = 2^k real blade coefficients, stored contiguously in this order
+ * (grade first, then lexicographic):
+ *     k = 1: (1, e1)
+ *     k = 2: (1, e1, e2, e12)
+ *     k = 3: (1, e1, e2, e3, e12, e13, e23, e123)
+ * Blade indices in this API are 0-based.
+ *
+ * Common conventions
+ *  - Every tensor is dense, row-major, fp32, with the blade index last.
+ *    Spatial indices are row-major with the first spatial axis slowest.
+ *  - Device pointers point to memory of the current HIP device.  The caller
+ *    owns every buffer; the library never allocates or frees device memory in
+ *    these calls and keeps no pointer after a call returns.
+ *  - Calls enqueue work on `stream` (a hipStream_t passed as void*; NULL is
+ *    the null stream) and return without synchronising.  Results are visible
+ *    once the stream has reached the work.
+ *  - Errors are returned, never raised: argument checks happen before any
+ *    work is enqueued, and on an argument error the output is left untouched.
+ *    CLIFF_EDEVICE reports a HIP launch error (hipGetLastError) after the
+ *    launch; the output content is then undefined.
+ *  - Thread safety: calls may be made concurrently from several host threads.
+ */
+#ifndef CLIFFCONV_H
+#define CLIFFCONV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CLIFF_OK = 0,
+    CLIFF_EINVAL = 1,       /* null pointer, bad k / signature / act descriptor */
+    CLIFF_ESHAPE = 2,       /* non-positive size, d_filter > d_image, overflow */
+    CLIFF_EALIGN = 3,       /* tensor pointer not 16-byte aligned */
+    CLIFF_EOVERLAP = 4,     /* output memory overlaps an input */
+    CLIFF_EUNSUPPORTED = 5, /* valid request this build cannot run */
+    CLIFF_EDEVICE = 6       /* HIP reported an error */
+} cliff_status;
+
+/* Gate aggregation of Algorithm 3. */
+typedef enum {
+    CLIFF_AGG_LINEAR = 0, /* s = sum_t input[blade_idx[t]] * weight[c, t] + bias[c] */
+    CLIFF_AGG_SUM = 1,    /* s = sum_t input[blade_idx[t]]                       */
+    CLIFF_AGG_MEAN = 2    /* s = (sum_t input[blade_idx[t]]) / K                 */
+} cliff_agg;
+
+/*
+ * Multivector activation descriptor (paper, Algorithm 3): for every
+ * multivector of channel c the gate s is formed from the K selected blades
+ * and every blade j is scaled, out[j] = in[j] * sigmoid(s), with
+ * sigmoid(s) = 1 / (1 + exp(-s)).
+ *   mode       cliff_agg
+ *   K          number of gating blades, 1 <= K <= N_B
+ *   blade_idx  K distinct 0-based blade indices (entries past K ignored);
+ *              host memory, read during the call only
+ *   weight     device [C, K] fp32, Linear only (ignored otherwise)
+ *   bias       device [C] fp32, Linear only (ignored otherwise)
+ * Spatial positions share the channel's weight and bias.
+ */
+typedef struct {
+    int32_t mode;
+    int32_t K;
+    int32_t blade_idx[8];
+    const float* weight;
+    const float* bias;
+} cliff_act_desc;
+
+/*
+ * k-D Clifford convolution (paper, Algorithm 1), no padding, unit stride, no
+ * dilation, followed by the bias add and, if `act` is not NULL, the
+ * multivector activation applied to the result:
+ *
+ *   output[b, co, p] = act( sum_{ci} sum_{q in [0, d_filter)^k}
+ *                               filters[ci, co, q] * input[b, ci, p + q]
+ *                           + bias[co] )
+ *
+ * where * is the geometric product with the filter on the left, and
+ * p ranges over [0, d_out)^k with d_out = d_image - d_filter + 1.
+ *
+ *   k         1, 2 or 3 (N_B = 2^k).  k = 2 and 3 run on the matrix cores;
+ *             k = 1 runs on a plain per-output kernel.
+ *   g         host int8[k], each in {-1, 0, +1}, not all 0
+ *   input     device [B, C_in, d_image^k, N_B]
+ *   filters   device [C_in, C_out, d_filter^k, N_B]
+ *   bias      device [C_out, N_B], or NULL for zero
+ *   output    device [B, C_out, d_out^k, N_B]; must not overlap any input
+ *   act       NULL, or the activation to fuse (weight [C_out, K], bias [C_out])
+ *   stream    hipStream_t or NULL
+ * Alignment: input, filters, bias and output 16-byte aligned (CLIFF_EALIGN);
+ * act->weight and act->bias 4-byte aligned.
+ * Sizes: B, C_in, C_out, d_filter >= 1, d_image >= d_filter (CLIFF_ESHAPE);
+ * every tensor must hold fewer than 2^40 elements.
+ * B = 0 is accepted and enqueues nothing.
+ */
+cliff_status clifford_conv_nd(int k, const int8_t* g, int64_t B, int64_t C_in,
+                              int64_t C_out, int64_t d_image, int64_t d_filter,
+                              const float* input, const float* filters,
+                              const float* bias, float* output,
+                              const cliff_act_desc* act, void* stream);
+
+/* Kernel choice for clifford_conv_nd_algo. */
+typedef enum {
+    CLIFF_ALGO_AUTO = 0,   /* what clifford_conv_nd does */
+    CLIFF_ALGO_DIRECT = 1, /* one thread per output multivector, fp32 FMA */
+    CLIFF_ALGO_MFMA = 2    /* implicit GEMM on fp32 MFMA (k = 2, 3 only) */
+} cliff_algo;
+
+/*
+ * Same operation and contract as clifford_conv_nd, with the kernel family
+ * forced (CLIFF_EUNSUPPORTED if that family cannot run the request).  For
+ * tests and benchmarks that compare the two families.
+ */
+cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
+                                   int64_t C_in, int64_t C_out, int64_t d_image,
+                                   int64_t d_filter, const float* input,
+                                   const float* filters, const float* bias,
+                                   float* output, const cliff_act_desc* act,
+                                   void* stream, int algo);
+
+/*
+ * Standalone multivector activation (paper, Algorithm 3).
+ *   nb      N_B in {2, 4, 8}
+ *   input   device [B, C, P, N_B]   (P positions per channel; P = 1 gives
+ *           the paper's [B, C, N_B])
+ *   output  device [B, C, P, N_B]; may equal input (in place) but must not
+ *           overlap it otherwise
+ * act must not be NULL; B, C, P >= 1 (B = 0 enqueues nothing).
+ * Alignment: input and output 16-byte aligned.
+ */
+cliff_status multivector_act(int nb, int64_t B, int64_t C, int64_t P,
+                             const cliff_act_desc* act, const float* input,
+                             float* output, void* stream);
+
+/*
+ * Host-side multiplication table the kernels are driven by (paper,
+ * Background, "Clifford Algebra"), for output blade i and input blade j:
+ *     (w * x)_i = sum_j sign[i*N_B + j] * w_{src[i*N_B + j]} * x_j
+ * i.e. e_{src} e_j = sign * e_i.  src and sign are caller-owned host arrays
+ * of N_B*N_B entries; sign is in {-1, 0, +1}.  No device work.
+ */
+cliff_status cliffconv_cayley_table(int k, const int8_t* g, int8_t* src,
+                                    int8_t* sign);
+
+/* Static, human-readable name of a status code. */
+const char* cliffconv_status_string(cliff_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLIFFCONV_H */

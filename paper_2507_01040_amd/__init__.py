@@ -1,0 +1,221 @@
+"""Python binding of libcliffconv.so, the MI355X (gfx950) Clifford
+convolution library.
+
+The entry points carry the names of the C ABI in include/cliffconv.h and only
+marshal arguments; every step of the computation runs in the library's HIP
+kernels.  torch is used for device memory and the current stream only.  The
+library is built in-tree by ``paper_2507_01040_amd.build`` (or
+``__graft_entry__.build()``); importing this module does not build it, and
+every call raises if it is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcliffconv.so")
+
+CLIFF_OK, CLIFF_EINVAL, CLIFF_ESHAPE, CLIFF_EALIGN = 0, 1, 2, 3
+CLIFF_EOVERLAP, CLIFF_EUNSUPPORTED, CLIFF_EDEVICE = 4, 5, 6
+STATUS_NAMES = {0: "CLIFF_OK", 1: "CLIFF_EINVAL", 2: "CLIFF_ESHAPE",
+                3: "CLIFF_EALIGN", 4: "CLIFF_EOVERLAP",
+                5: "CLIFF_EUNSUPPORTED", 6: "CLIFF_EDEVICE"}
+AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
+ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
+
+EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "multivector_act",
+            "cliffconv_cayley_table", "cliffconv_status_string")
+
+
+class CliffActDesc(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("blade_idx", ctypes.c_int32 * 8),
+                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+
+
+class CliffError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (%s)" % (where, STATUS_NAMES.get(status, status),
+                                          status_string(status)))
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Loads the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            "libcliffconv.so is not built (%s); run __graft_entry__.build()" % path)
+    lib = ctypes.CDLL(path)
+    i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    conv_args = [i32, vp, i64, i64, i64, i64, i64, vp, vp, vp, vp,
+                 ctypes.POINTER(CliffActDesc), vp]
+    lib.clifford_conv_nd.argtypes = conv_args
+    lib.clifford_conv_nd_algo.argtypes = conv_args + [i32]
+    lib.multivector_act.argtypes = [i32, i64, i64, i64,
+                                    ctypes.POINTER(CliffActDesc), vp, vp, vp]
+    lib.cliffconv_cayley_table.argtypes = [i32, vp, vp, vp]
+    lib.cliffconv_status_string.argtypes = [i32]
+    lib.cliffconv_status_string.restype = ctypes.c_char_p
+    for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "multivector_act",
+                 "cliffconv_cayley_table"):
+        getattr(lib, name).restype = i32
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().cliffconv_status_string(status).decode()
+
+
+def _g_array(g: Sequence[int]):
+    arr = (ctypes.c_int8 * max(len(g), 1))(*[int(v) for v in g])
+    return arr
+
+
+def make_act_desc(mode: int, blades: Sequence[int], weight_ptr: int = 0,
+                  bias_ptr: int = 0) -> CliffActDesc:
+    d = CliffActDesc()
+    d.mode = int(mode)
+    d.K = len(blades)
+    for t, b in enumerate(blades[:8]):
+        d.blade_idx[t] = int(b)
+    d.weight = weight_ptr or None
+    d.bias = bias_ptr or None
+    return d
+
+
+# ---------------------------------------------------------------------------
+# Raw C-ABI calls (pointers are ints, as from torch.Tensor.data_ptr()).
+# ---------------------------------------------------------------------------
+
+def clifford_conv_nd(k: int, g: Sequence[int], B: int, C_in: int, C_out: int,
+                     d_image: int, d_filter: int, input_ptr: int,
+                     filters_ptr: int, bias_ptr: int, output_ptr: int,
+                     act: Optional[CliffActDesc] = None, stream: int = 0) -> int:
+    """Returns the cliff_status of the C call."""
+    return load().clifford_conv_nd(
+        k, _g_array(g), B, C_in, C_out, d_image, d_filter, input_ptr or None,
+        filters_ptr or None, bias_ptr or None, output_ptr or None,
+        ctypes.byref(act) if act is not None else None, stream or None)
+
+
+def clifford_conv_nd_algo(k: int, g: Sequence[int], B: int, C_in: int,
+                          C_out: int, d_image: int, d_filter: int,
+                          input_ptr: int, filters_ptr: int, bias_ptr: int,
+                          output_ptr: int, act: Optional[CliffActDesc] = None,
+                          stream: int = 0, algo: int = ALGO_AUTO) -> int:
+    return load().clifford_conv_nd_algo(
+        k, _g_array(g), B, C_in, C_out, d_image, d_filter, input_ptr or None,
+        filters_ptr or None, bias_ptr or None, output_ptr or None,
+        ctypes.byref(act) if act is not None else None, stream or None, algo)
+
+
+def multivector_act(nb: int, B: int, C: int, P: int, act: CliffActDesc,
+                    input_ptr: int, output_ptr: int, stream: int = 0) -> int:
+    return load().multivector_act(nb, B, C, P, ctypes.byref(act),
+                                  input_ptr or None, output_ptr or None,
+                                  stream or None)
+
+
+def cliffconv_cayley_table(k: int, g: Sequence[int]):
+    """(src, sign) as nested lists [N_B][N_B]; raises on bad arguments."""
+    nb = 1 << k
+    src = (ctypes.c_int8 * (nb * nb))()
+    sign = (ctypes.c_int8 * (nb * nb))()
+    st = load().cliffconv_cayley_table(k, _g_array(g), src, sign)
+    if st != CLIFF_OK:
+        raise CliffError(st, "cliffconv_cayley_table")
+    return ([[src[i * nb + j] for j in range(nb)] for i in range(nb)],
+            [[sign[i * nb + j] for j in range(nb)] for i in range(nb)])
+
+
+# ---------------------------------------------------------------------------
+# torch-tensor conveniences (device memory and stream plumbing only).
+# ---------------------------------------------------------------------------
+
+def _check_dev(t, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError("%s must be contiguous float32" % name)
+
+
+def _stream_ptr(stream) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
+            out=None, stream=None, algo: int = ALGO_AUTO):
+    """Clifford convolution of GPU tensors x [B,C_in,d^k,N_B] and filters
+    [C_in,C_out,d_f^k,N_B] with bias [C_out,N_B] (or None); ``act`` is None or
+    (mode, blades, weight [C_out,K] or None, bias [C_out] or None).  Returns
+    the output tensor [B,C_out,d_out^k,N_B] (allocated with torch unless
+    ``out`` is given)."""
+    import torch
+    k = len(g)
+    _check_dev(x, "x")
+    _check_dev(filters, "filters")
+    if bias is not None:
+        _check_dev(bias, "bias")
+    B, C_in, d_image = x.shape[0], x.shape[1], x.shape[2]
+    C_out, d_filter = filters.shape[1], filters.shape[2]
+    d_out = d_image - d_filter + 1
+    shape = (B, C_out) + (d_out,) * k + (1 << k,)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=x.device)
+    desc = None
+    if act is not None:
+        mode, blades, aw, ab = act
+        desc = make_act_desc(mode, blades, aw.data_ptr() if aw is not None else 0,
+                             ab.data_ptr() if ab is not None else 0)
+    st = clifford_conv_nd_algo(k, g, B, C_in, C_out, d_image, d_filter,
+                               x.data_ptr(), filters.data_ptr(),
+                               bias.data_ptr() if bias is not None else 0,
+                               out.data_ptr(), desc, _stream_ptr(stream), algo)
+    if st != CLIFF_OK:
+        raise CliffError(st, "clifford_conv_nd")
+    return out
+
+
+def act_nd(x, mode: int, blades: Sequence[int], weight=None, bias=None,
+           out=None, stream=None):
+    """Multivector activation of a GPU tensor [B, C, (positions...), N_B]."""
+    import torch
+    _check_dev(x, "x")
+    B, C, nb = x.shape[0], x.shape[1], x.shape[-1]
+    P = 1
+    for s in x.shape[2:-1]:
+        P *= s
+    if out is None:
+        out = torch.empty_like(x)
+    desc = make_act_desc(mode, blades, weight.data_ptr() if weight is not None else 0,
+                         bias.data_ptr() if bias is not None else 0)
+    st = multivector_act(nb, B, C, P, desc, x.data_ptr(), out.data_ptr(),
+                         _stream_ptr(stream))
+    if st != CLIFF_OK:
+        raise CliffError(st, "multivector_act")
+    return out
+
+
+def block_forward(x, layers, g: Sequence[int], outs=None, stream=None):
+    """Block composition: conv (+ fused bias and activation) for each layer
+    in turn, the intermediate kept in HBM in the blade-last layout.
+    ``layers`` is a sequence of (filters, bias, act) with act None or
+    (mode, blades, weight or None, bias or None); ``outs`` optionally gives
+    preallocated outputs per layer."""
+    y = x
+    for li, (f, b, a) in enumerate(layers):
+        y = conv_nd(y, f, b, g, act=a, out=None if outs is None else outs[li],
+                    stream=stream)
+    return y

@@ -1,0 +1,67 @@
+// Shared definitions of the HIP kernels and the host dispatch code.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cliffconv.h"
+
+namespace cliff {
+
+// Blade storage order is grade-then-lexicographic; inside the kernels a blade
+// is handled as a bitmask over the generators (bit t-1 set <=> e_t present).
+// The two orders differ only for k = 3, where slot 3 holds e3 (mask 4) and
+// slot 4 holds e12 (mask 3); the map is its own inverse.
+__host__ __device__ constexpr int blade_perm(int nb, int v)
+{
+    return nb == 8 ? (v == 3 ? 4 : (v == 4 ? 3 : v)) : v;
+}
+
+// For output blade i and input blade j (storage order), the filter blade whose
+// product with e_j lands on e_i: e_src e_j = +-e_i, src = i XOR j on bitmasks.
+__host__ __device__ constexpr int src_blade(int nb, int i, int j)
+{
+    return blade_perm(nb, blade_perm(nb, i) ^ blade_perm(nb, j));
+}
+
+// Signs of the table, bit e = i * nb + j: neg set => -1, zero set => 0,
+// neither => +1.
+struct SignMasks {
+    uint64_t neg;
+    uint64_t zero;
+};
+
+__host__ __device__ inline float sign_of(const SignMasks& s, int e)
+{
+    if ((s.zero >> e) & 1ull) return 0.0f;
+    return ((s.neg >> e) & 1ull) ? -1.0f : 1.0f;
+}
+
+struct ActParams {
+    int mode;  // -1: no activation
+    int K;
+    int idx[8];
+    const float* weight;
+    const float* bias;
+};
+
+struct ConvProblem {
+    int k, nb;
+    int64_t B, C_in, C_out, d_image, d_filter, d_out;
+    const float* x;
+    const float* w;
+    const float* bias;
+    float* y;
+    SignMasks sign;
+    ActParams act;
+};
+
+// host-side launchers (defined in the .hip files)
+cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
+// Returns CLIFF_EUNSUPPORTED without launching when no MFMA tiling fits.
+cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream);
+cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P,
+                        const ActParams& a, const float* x, float* y,
+                        hipStream_t stream);
+
+}  // namespace cliff

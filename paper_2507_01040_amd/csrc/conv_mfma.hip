@@ -1,0 +1,394 @@
+// k-D Clifford convolution (paper, Algorithm 1) as an implicit GEMM on the
+// CDNA4 fp32 matrix cores (v_mfma_f32_16x16x4_f32), k = 2 and 3.
+//
+// GEMM view.  With the blades folded into the channels the layer is a dense
+// contraction
+//     Y[(co, i), m] = sum_{q, ci, j} E[(co, i), (q, ci, j)] * X[(q, ci, j), m]
+// with m an output position (b, p), X[(q, ci, j), m] = input[b, ci, p + q, j]
+// and E the Clifford kernel expansion E[(co,i),(q,ci,j)] =
+// s[i][j] * filters[ci, co, q, src(i, j)] (the paper's "Baseline" builds E in
+// memory, with N_B-fold duplication; here it is never materialised: every
+// lane of an MFMA A-fragment owns one fixed (i, j) pair, so it reads the raw
+// filter blade src(i, j) from LDS and applies its sign in a register).
+//
+// MFMA roles.  A (16x4) = E rows (4 output channels x 4 blades for N_B = 4,
+// 2 x 8 for N_B = 8) by 4 input blades j; B (4x16) = 4 input blades by 16
+// consecutive output positions; D (16x16) leaves every lane with 4
+// consecutive output blades of one (channel, position), so results go to HBM
+// as 16-byte stores in the blade-last layout and the activation gate needs
+// at most one cross-lane exchange.
+//
+// Work decomposition.  The flattened output positions m in [0, B d_out^k)
+// are cut into blocks of P consecutive positions (they may span rows, planes
+// and batch entries); a workgroup computes P positions x CO_WG output
+// channels.  The K loop runs over "stages": one input channel (2D) or one
+// (input channel, filter plane qz) pair (3D).  For each stage the workgroup
+// stages in LDS (double-buffered through registers):
+//   * the slab: every input row the block's outputs touch for this stage,
+//     rows of d_image multivectors, kept blade-packed ([row][x][4] for N_B = 4,
+//     [row][half][x][4] for N_B = 8 so that a fragment read is 64 consecutive
+//     words);
+//   * the raw filters [co][tap][blade] of this stage (no expansion).
+#include <algorithm>
+
+#include "common.hpp"
+#include "epilogue.hpp"
+
+namespace cliff {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+struct MfmaArgs {
+    const float* x;
+    const float* w;
+    const float* bias;
+    float* y;
+    int C_in, C_out, D, Do, df;
+    int M;          // number of output positions B * d_out^k
+    int npos;       // d_out^k
+    int n_stage;    // C_in (k = 2) or C_in * d_filter (k = 3)
+    int n_co_blk, n_blk;
+    int slab_floats;   // LDS floats reserved for the slab in one buffer
+    int stage_floats;  // slab + filters, one buffer
+    SignMasks sign;
+    ActParams act;
+};
+
+template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS>
+__global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
+{
+    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int CPT = 16 / NB;  // output channels per 16-row tile
+    constexpr int CO_WG = WCO * MW * CPT;
+    constexpr int P = WPOS * NW * 16;
+    constexpr int NH = NB / 4;  // groups of 4 input blades (MFMA K = 4)
+
+    extern __shared__ f4 smem4[];
+    float* smem = reinterpret_cast<float*>(smem4);
+
+    const int df = DF > 0 ? DF : a.df;
+    const int taps2 = df * df;
+    const int taps_full = KD == 2 ? taps2 : taps2 * df;
+    const int D = a.D, Do = a.Do;
+    const int row_floats = D * NB;
+    const int row_f4 = row_floats / 4;
+    const int tid = threadIdx.x;
+
+    // Workgroups are dispatched round-robin over the 8 XCDs; renumber them so
+    // each XCD (own L2) works through a contiguous run of position blocks,
+    // whose input slabs overlap.
+    const int bid = blockIdx.x;
+    const int per = a.n_blk / 8, rem = a.n_blk % 8;
+    const int xcd = bid % 8, slot = bid / 8;
+    const int tile = xcd < rem ? xcd * (per + 1) + slot
+                               : rem * (per + 1) + (xcd - rem) * per + slot;
+    const int co_blk = tile % a.n_co_blk;
+    const int pos_blk = tile / a.n_co_blk;
+    const int co0 = co_blk * CO_WG;
+    const int m0 = pos_blk * P;
+    const int m_end = min(m0 + P, a.M);
+
+    // Slab geometry: output rows r0..r1 (rows of d_out positions), planes
+    // pl0..pl1 (2D: batch entry; 3D: (batch, z)).  Each plane contributes its
+    // output rows plus d_filter - 1 halo rows; full middle planes contribute
+    // all d_image rows.
+    const int r0 = m0 / Do, r1 = (m_end - 1) / Do;
+    const int pl0 = r0 / Do, pl1 = r1 / Do;
+    const int ylo0 = r0 - pl0 * Do;
+    const int len0 = pl0 == pl1 ? (r1 - r0) + df : D - ylo0;
+    const int n_rows = pl0 == pl1 ? len0
+                                  : len0 + (pl1 - pl0 - 1) * D + (r1 - pl1 * Do) + df;
+
+    // Staging slots of this thread (fixed for all stages).
+    const int slab_f4 = n_rows * row_f4;
+    const int wq_f4 = taps2 * NB / 4;
+    const int total_f4 = slab_f4 + CO_WG * wq_f4;
+    int64_t goff[SLOTS];
+    int ldst[SLOTS];
+    int kind[SLOTS];  // 0 input, 1 filter, 2 zero filter (co >= C_out), 3 idle
+#pragma unroll
+    for (int t = 0; t < SLOTS; ++t) {
+        const int f = tid + t * NT;
+        goff[t] = 0;
+        ldst[t] = 0;
+        kind[t] = 3;
+        if (f < slab_f4) {
+            const int row = f / row_f4;
+            const int col = f - row * row_f4;
+            int pl, yin;
+            if (row < len0) {
+                pl = pl0;
+                yin = ylo0 + row;
+            } else {
+                const int s2 = row - len0;
+                pl = pl0 + 1 + s2 / D;
+                yin = s2 - (s2 / D) * D;
+            }
+            int64_t base;
+            if (KD == 2) {
+                base = ((int64_t)pl * a.C_in * D + yin) * row_floats;
+            } else {
+                const int b = pl / Do, z = pl - (pl / Do) * Do;
+                base = (((int64_t)b * a.C_in * D + z) * D + yin) * row_floats;
+            }
+            goff[t] = base + col * 4;
+            ldst[t] = row * row_floats +
+                      (NB == 8 ? (col & 1) * D * 4 + (col >> 1) * 4 : col * 4);
+            kind[t] = 0;
+        } else if (f < total_f4) {
+            const int e = f - slab_f4;
+            const int co_l = e / wq_f4;
+            const int r4 = e - co_l * wq_f4;
+            const int co = co0 + co_l;
+            goff[t] = (int64_t)co * taps_full * NB + r4 * 4;
+            ldst[t] = a.slab_floats + co_l * taps2 * NB + r4 * 4;
+            kind[t] = co < a.C_out ? 1 : 2;
+        }
+    }
+
+    const int64_t x_cstride = (int64_t)D * D * (KD == 3 ? D : 1) * NB;
+    const int64_t w_cstride = (int64_t)a.C_out * taps_full * NB;
+    f4 stg[SLOTS];
+    auto load_stage = [&](int s) {
+        int ci = s, qz = 0;
+        if (KD == 3) {
+            ci = s / df;
+            qz = s - ci * df;
+        }
+        const int64_t xs = ci * x_cstride + (int64_t)qz * D * D * NB;
+        const int64_t ws = ci * w_cstride + (int64_t)qz * taps2 * NB;
+#pragma unroll
+        for (int t = 0; t < SLOTS; ++t) {
+            if (kind[t] == 0)
+                stg[t] = *reinterpret_cast<const f4*>(a.x + goff[t] + xs);
+            else if (kind[t] == 1)
+                stg[t] = *reinterpret_cast<const f4*>(a.w + goff[t] + ws);
+            else
+                stg[t] = f4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    auto store_stage = [&](int buf) {
+        float* base = smem + buf * a.stage_floats;
+#pragma unroll
+        for (int t = 0; t < SLOTS; ++t)
+            if (kind[t] != 3) *reinterpret_cast<f4*>(base + ldst[t]) = stg[t];
+    };
+
+    // Per-lane constants of the MFMA fragments.
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wco = wave % WCO;
+    const int wpos = wave / WCO;
+    const int mrow = lane & 15;
+    const int kk = lane >> 4;
+
+    // A: row mrow = (output channel co_a, output blade i_a), column kk =
+    // input blade j = 4h + kk.
+    const int co_a = mrow / NB;
+    const int i_a = mrow % NB;
+    int wofs[NH];
+    float sg[NH];
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+        const int j = 4 * h + kk;
+        sg[h] = sign_of(a.sign, i_a * NB + j);
+        wofs[h] = a.slab_floats + (wco * MW * CPT + co_a) * taps2 * NB +
+                  src_blade(NB, i_a, j);
+    }
+    // B: row kk = input blade, column mrow = output position.
+    int xoff[NW];
+#pragma unroll
+    for (int nw = 0; nw < NW; ++nw) {
+        int m = m0 + (wpos * NW + nw) * 16 + mrow;
+        m = min(m, m_end - 1);  // tail lanes read a valid position, never stored
+        const int r = m / Do;
+        const int xx = m - r * Do;
+        const int pl = r / Do;
+        const int yy = r - pl * Do;
+        const int srow = pl == pl0 ? yy - ylo0 : len0 + (pl - pl0 - 1) * D + yy;
+        xoff[nw] = srow * row_floats + xx * 4 + kk;
+    }
+
+    f4 acc[MW][NW];
+#pragma unroll
+    for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+        for (int nw = 0; nw < NW; ++nw) acc[mw][nw] = f4{0.f, 0.f, 0.f, 0.f};
+
+    const int wtile = CPT * taps2 * NB;  // LDS floats between channel tiles
+    auto compute = [&](int buf) {
+        const float* S = smem + buf * a.stage_floats;
+#pragma unroll
+        for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
+            for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
+                const int qy_ = DF > 0 ? qy : qyr;
+#pragma unroll
+                for (int qx = 0; qx < (DF > 0 ? DF : 1); ++qx) {
+                    for (int qxr = 0; qxr < (DF > 0 ? 1 : df); ++qxr) {
+                        const int qx_ = DF > 0 ? qx : qxr;
+                        const int tap = qy_ * df + qx_;
+#pragma unroll
+                        for (int h = 0; h < NH; ++h) {
+                            float av[MW], bv[NW];
+#pragma unroll
+                            for (int mw = 0; mw < MW; ++mw)
+                                av[mw] = S[wofs[h] + mw * wtile + tap * NB] * sg[h];
+#pragma unroll
+                            for (int nw = 0; nw < NW; ++nw)
+                                bv[nw] = S[xoff[nw] + qy_ * row_floats + h * D * 4 +
+                                           qx_ * 4];
+#pragma unroll
+                            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                                for (int nw = 0; nw < NW; ++nw)
+                                    acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                                        av[mw], bv[nw], acc[mw][nw], 0, 0, 0);
+                        }
+                    }
+                }
+            }
+        }
+    };
+
+    // Main loop: one barrier per stage; the next stage's global loads are in
+    // flight while the current one is multiplied.
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+    for (int s = 0; s < a.n_stage; ++s) {
+        const bool more = s + 1 < a.n_stage;
+        if (more) load_stage(s + 1);
+        compute(s & 1);
+        if (more) store_stage((s + 1) & 1);
+        __syncthreads();
+    }
+
+    // Epilogue: bias, optional multivector activation, 16-byte stores.
+    // D fragment: lane holds rows 4*kk + r of the tile, i.e. output channel
+    // co_o and blades i0..i0+3, for position column mrow.
+    const int co_o = NB == 4 ? kk : (kk >> 1);
+    const int i0 = NB == 4 ? 0 : 4 * (kk & 1);
+    const bool has_act = a.act.mode >= 0;
+    int gslot[4] = {-1, -1, -1, -1};
+    if (has_act) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gslot[r] = gate_slot(a.act, i0 + r);
+    }
+#pragma unroll
+    for (int mw = 0; mw < MW; ++mw) {
+        const int co = co0 + (wco * MW + mw) * CPT + co_o;
+        const bool cvalid = co < a.C_out;
+        f4 bb = f4{0.f, 0.f, 0.f, 0.f};
+        if (cvalid && a.bias) bb = *reinterpret_cast<const f4*>(a.bias + co * NB + i0);
+        float cf[4] = {0.f, 0.f, 0.f, 0.f};
+        if (has_act && cvalid) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) cf[r] = gate_coef(a.act, gslot[r], co);
+        }
+#pragma unroll
+        for (int nw = 0; nw < NW; ++nw) {
+            const int m = m0 + (wpos * NW + nw) * 16 + mrow;
+            f4 v = acc[mw][nw] + bb;
+            if (has_act) {
+                float part = cf[0] * v[0] + cf[1] * v[1] + cf[2] * v[2] + cf[3] * v[3];
+                if (NB == 8) part += __shfl_xor(part, 16);
+                const float gate = cvalid ? gate_sigmoid(a.act, part, co) : 0.f;
+                v *= gate;
+            }
+            if (cvalid && m < m_end) {
+                const int b = m / a.npos;
+                const int sp = m - b * a.npos;
+                *reinterpret_cast<f4*>(a.y + (((int64_t)b * a.C_out + co) * a.npos + sp) * NB +
+                                       i0) = v;
+            }
+        }
+    }
+}
+
+struct TileCfg {
+    int wco, wpos, mw, nw;
+};
+
+template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW>
+cliff_status run(const ConvProblem& p, hipStream_t stream)
+{
+    constexpr int SLOTS = 8;
+    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int CPT = 16 / NB;
+    constexpr int CO_WG = WCO * MW * CPT;
+    constexpr int P = WPOS * NW * 16;
+    const int64_t D = p.d_image, Do = p.d_out, df = p.d_filter;
+    int64_t npos = 1;
+    for (int t = 0; t < KD; ++t) npos *= Do;
+    const int64_t M = p.B * npos;
+    const int64_t n_pos_blk = (M + P - 1) / P;
+    const int64_t n_co_blk = (p.C_out + CO_WG - 1) / CO_WG;
+    const int64_t n_blk = n_pos_blk * n_co_blk;
+    if (M >= (1ll << 31) || n_blk >= (1ll << 31) || D * D * NB >= (1 << 24))
+        return CLIFF_EUNSUPPORTED;
+    // Upper bound of the slab rows of any block.
+    const int64_t total_rows = M / Do;
+    const int64_t R = std::min<int64_t>((P - 1) / Do + 2, total_rows);
+    const int64_t planes = std::min<int64_t>(R, (R - 1) / Do + 2);
+    const int64_t rows_max = R + planes * (df - 1);
+    const int64_t slab_floats = rows_max * D * NB;
+    const int64_t w_floats = CO_WG * df * df * NB;
+    const int64_t stage_floats = slab_floats + w_floats;
+    const int64_t lds_bytes = 2 * stage_floats * 4;
+    if (lds_bytes > 64 * 1024) return CLIFF_EUNSUPPORTED;
+    if ((slab_floats + w_floats) / 4 > (int64_t)SLOTS * NT) return CLIFF_EUNSUPPORTED;
+
+    MfmaArgs a;
+    a.x = p.x;
+    a.w = p.w;
+    a.bias = p.bias;
+    a.y = p.y;
+    a.C_in = (int)p.C_in;
+    a.C_out = (int)p.C_out;
+    a.D = (int)D;
+    a.Do = (int)Do;
+    a.df = (int)df;
+    a.M = (int)M;
+    a.npos = (int)npos;
+    a.n_stage = (int)(KD == 2 ? p.C_in : p.C_in * df);
+    a.n_co_blk = (int)n_co_blk;
+    a.n_blk = (int)n_blk;
+    a.slab_floats = (int)slab_floats;
+    a.stage_floats = (int)stage_floats;
+    a.sign = p.sign;
+    a.act = p.act;
+    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS>),
+                       dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
+    return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
+}
+
+template <int KD, int NB, int DF>
+cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
+{
+    // wide: all (or half) of the output channels per workgroup, 128 positions;
+    // narrow: few channels, 256 positions (small C_out).
+    constexpr int CO_WIDE = 2 * 8 * (16 / NB);
+    if (p.C_out * 2 > CO_WIDE) {
+        const cliff_status s = run<KD, NB, DF, 2, 2, 8, 4>(p, stream);
+        if (s != CLIFF_EUNSUPPORTED) return s;
+    }
+    return run<KD, NB, DF, 1, 4, 2, 4>(p, stream);
+}
+
+}  // namespace
+
+cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream)
+{
+    if (p.k == 2) {
+        if (p.d_filter == 3) return run_shape<2, 4, 3>(p, stream);
+        return run_shape<2, 4, 0>(p, stream);
+    }
+    if (p.k == 3) {
+        if (p.d_filter == 3) return run_shape<3, 8, 3>(p, stream);
+        return run_shape<3, 8, 0>(p, stream);
+    }
+    return CLIFF_EUNSUPPORTED;
+}
+
+}  // namespace cliff

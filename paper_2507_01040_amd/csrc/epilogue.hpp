@@ -1,0 +1,40 @@
+// Device helpers for the multivector activation (paper, Algorithm 3), shared
+// by the fused convolution epilogues and the standalone activation kernel.
+#pragma once
+
+#include "common.hpp"
+
+namespace cliff {
+
+// Position of blade `blade` in the gate's blade list, or -1.
+__device__ inline int gate_slot(const ActParams& act, int blade)
+{
+    int slot = -1;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        if (t < act.K && act.idx[t] == blade) slot = t;
+    return slot;
+}
+
+// Gate weight of `blade` for channel c: Linear -> weight[c, slot], Sum/Mean
+// -> 1 for the selected blades; 0 for blades outside the subset.
+__device__ inline float gate_coef(const ActParams& act, int slot, int c)
+{
+    if (slot < 0) return 0.0f;
+    return act.mode == CLIFF_AGG_LINEAR ? act.weight[(int64_t)c * act.K + slot]
+                                        : 1.0f;
+}
+
+// Gate value s from the full aggregated sum (Linear adds the channel bias,
+// Mean divides by K), then sigmoid(s) = 1 / (1 + exp(-s)).
+__device__ inline float gate_sigmoid(const ActParams& act, float sum, int c)
+{
+    float s = sum;
+    if (act.mode == CLIFF_AGG_LINEAR)
+        s = s + act.bias[c];
+    else if (act.mode == CLIFF_AGG_MEAN)
+        s = s / (float)act.K;
+    return 1.0f / (1.0f + __expf(-s));
+}
+
+}  // namespace cliff

@@ -1,0 +1,118 @@
+"""Full-size parity on the five benchmark workloads, run through the C ABI in
+the launch configuration the benchmark times (clifford_conv_nd, automatic
+kernel choice, activation fused into the convolution for the blocks).
+
+The oracle cannot afford every output at these sizes, so it checks:
+  * the 2D tiny workload in full;
+  * single convolutions: sampled outputs computed one by one by the oracle
+    (every batch entry, first and last channels, all four/eight borders of the
+    output grid, plus seeded random positions);
+  * blocks (conv -> act -> conv -> act): spatial patches; by translation
+    equivariance (no padding) the block applied to a cropped input equals the
+    same window of the full output, so the oracle runs the whole block, in
+    fp64 end to end, on crops at the corners, edges and interior.
+Gate: normwise relative error <= 1e-4 (see test_parity_gpu).
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2507_01040_amd as P
+import workloads as W
+from gpu_util import assert_parity, dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_block(w: W.Workload, x, params):
+    """The benchmark's pass: every layer through clifford_conv_nd with the
+    bias and (if any) activation fused."""
+    xt = dev(x)
+    ts = []
+    for li, (shape, act) in enumerate(zip(w.layers, w.acts)):
+        p = params[li]
+        a = None
+        if act is not None:
+            a = (act.mode, act.blades,
+                 dev(p.act_weight) if p.act_weight is not None else None,
+                 dev(p.act_bias) if p.act_bias is not None else None)
+        ts.append((dev(p.filters), dev(p.bias), a))
+    y = P.block_forward(xt, ts, w.layers[0].g)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def _sample_points(shape: W.ConvShape, n_random: int, seed: int):
+    k, Do = shape.k, shape.d_out
+    pts = []
+    edges = [0, Do - 1]
+    for b in range(shape.B):
+        for co in (0, shape.C_out - 1):
+            for c in itertools.product(edges, repeat=k):
+                pts.append((b, co, c))
+    rng = np.random.default_rng(seed)
+    for _ in range(n_random):
+        pts.append((int(rng.integers(shape.B)), int(rng.integers(shape.C_out)),
+                    tuple(int(v) for v in rng.integers(0, Do, k))))
+    bs = np.array([p[0] for p in pts])
+    cos = np.array([p[1] for p in pts])
+    flat = np.array([int(np.ravel_multi_index(p[2], (Do,) * k)) for p in pts])
+    return bs, cos, flat
+
+
+def test_c1_full():
+    w = W.WORKLOADS["c1_2d_tiny"]
+    x, ps = W.make_inputs(w)
+    y = _gpu_block(w, x, ps)
+    ref = oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g)
+    assert_parity(y, ref)
+
+
+@pytest.mark.parametrize("name", ["c2_2d_c64_d128", "c3_3d_c32_d32"])
+def test_single_conv_sampled(name):
+    w = W.WORKLOADS[name]
+    x, ps = W.make_inputs(w)
+    shape = w.layers[0]
+    y = _gpu_block(w, x, ps)
+    assert np.all(np.isfinite(y))
+    bs, cos, flat = _sample_points(shape, 3000, 5)
+    ref = oracle.conv_points(x, ps[0].filters, ps[0].bias, shape.g, bs, cos, flat)
+    got = y.reshape(shape.B, shape.C_out, -1, shape.nb)[bs, cos, flat]
+    e = assert_parity(got, ref, what=name)
+    print("%s sampled normwise error %.3e over %d outputs" % (name, e, len(bs)))
+
+
+def _patch_origins(d_final, ps, k, seed):
+    lo, hi = 0, d_final - ps
+    rng = np.random.default_rng(seed)
+    origins = [(lo,) * k, (hi,) * k, tuple([lo] * (k - 1) + [hi]),
+               tuple(int(v) for v in rng.integers(0, hi + 1, k))]
+    return origins
+
+
+@pytest.mark.parametrize("name,ps", [("c4_2d_block_c64_d130", 12),
+                                     ("c5_3d_block_c64_d36", 4)])
+def test_block_patches(name, ps):
+    w = W.WORKLOADS[name]
+    x, params = W.make_inputs(w)
+    y = _gpu_block(w, x, params)
+    assert np.all(np.isfinite(y))
+    k = w.layers[0].k
+    halo = sum(l.d_filter - 1 for l in w.layers)
+    d_final = w.layers[-1].d_out
+    layers = []
+    for p, a in zip(params, w.acts):
+        layers.append((p.filters, p.bias,
+                       None if a is None else (a.mode, a.blades, p.act_weight, p.act_bias)))
+    worst = 0.0
+    for b in (0, w.layers[0].B - 1):
+        for org in _patch_origins(d_final, ps, k, b):
+            crop = (slice(b, b + 1), slice(None)) + tuple(
+                slice(o, o + ps + halo) for o in org)
+            ref = oracle.block(x[crop], layers, w.layers[0].g)
+            win = (slice(b, b + 1), slice(None)) + tuple(slice(o, o + ps) for o in org)
+            worst = max(worst, assert_parity(y[win], ref, what="%s b=%d at %s" % (name, b, org)))
+    print("%s worst patch normwise error %.3e" % (name, worst))

@@ -1,0 +1,217 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on
+the same seeded inputs, element by element.
+
+Tolerance.  The GPU accumulates n = C_in N_B d_filter^k fp32 products per
+output blade in a different order than the oracle; the worst-case bound
+n * 2^-24 * sum|terms| is not small for large n (1.4e-4 relative at
+n = 2304), but the rounding errors of a long random-sign sum are a random
+walk, so the realised normwise error max|y - r| / max|r| stays near
+1e-6 at the full sizes and far below at these sizes; the gate is 1e-4
+normwise.  Outputs are NaN-prefilled so an unwritten element fails the check.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2507_01040_amd as P
+from gpu_util import assert_parity, dev, gpu_act, gpu_conv, normwise
+from workloads import AGG_LINEAR, AGG_MEAN, AGG_SUM, random_act_case, random_conv_case
+
+pytestmark = pytest.mark.gpu
+
+SIG2 = [g for g in itertools.product((-1, 0, 1), repeat=2) if any(g)]
+SIG3 = [(1, 1, 1), (-1, -1, -1), (1, -1, 0), (0, 1, -1), (1, 1, -1), (-1, 0, 0)]
+
+# (B, C_in, C_out, d_image, d_filter)
+SHAPES2 = [
+    (1, 1, 1, 5, 3),      # tiny, single tile, C < tile
+    (3, 3, 4, 11, 2),     # even filter
+    (8, 4, 4, 16, 3),     # the 2D tiny workload's shape
+    (2, 17, 3, 9, 5),     # large filter, odd channels
+    (3, 5, 70, 20, 3),    # two channel blocks, ragged positions
+    (1, 2, 9, 7, 1),      # pointwise (linear-layer-like)
+    (2, 3, 5, 6, 6),      # d_out = 1
+]
+SHAPES3 = [
+    (1, 1, 1, 4, 3),
+    (2, 3, 33, 12, 3),    # two channel blocks, ragged positions
+    (3, 2, 5, 7, 2),
+    (1, 4, 3, 9, 5),
+    (2, 2, 4, 3, 1),
+]
+
+
+def _case(seed, g, shape):
+    B, C_in, C_out, d_image, d_filter = shape
+    return random_conv_case(seed, len(g), g, B, C_in, C_out, d_image, d_filter)
+
+
+@pytest.mark.parametrize("algo", [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT],
+                         ids=["auto", "mfma", "direct"])
+@pytest.mark.parametrize("shape", SHAPES2, ids=str)
+def test_conv2d_parity(algo, shape):
+    g = (1, 1)
+    s, x, f, b = _case(100, g, shape)
+    y = _run_allow_unsupported(g, x, f, b, algo)
+    if y is None:
+        return
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(shape))
+
+
+def _run_allow_unsupported(g, x, f, b, algo, act=None):
+    """MFMA forced may legitimately refuse shapes whose slab does not fit."""
+    if algo != P.ALGO_MFMA:
+        return gpu_conv(g, x, f, b, act=act, algo=algo)
+    try:
+        return gpu_conv(g, x, f, b, act=act, algo=algo)
+    except AssertionError as e:
+        if "CLIFF_EUNSUPPORTED" in str(e):
+            return None
+        raise
+
+
+@pytest.mark.parametrize("algo", [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT],
+                         ids=["auto", "mfma", "direct"])
+@pytest.mark.parametrize("shape", SHAPES3, ids=str)
+def test_conv3d_parity(algo, shape):
+    g = (1, 1, 1)
+    s, x, f, b = _case(101, g, shape)
+    y = _run_allow_unsupported(g, x, f, b, algo)
+    if y is None:
+        return
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(shape))
+
+
+@pytest.mark.parametrize("g", SIG2 + SIG3, ids=str)
+def test_all_signatures(g):
+    shape = (2, 3, 6, 9, 3) if len(g) == 2 else (2, 3, 3, 6, 3)
+    s, x, f, b = _case(102, g, shape)
+    ref = oracle.conv_nd(x, f, b, g)
+    for algo in (P.ALGO_MFMA, P.ALGO_DIRECT):
+        assert_parity(gpu_conv(g, x, f, b, algo=algo), ref, what="%s algo %d" % (g, algo))
+
+
+@pytest.mark.parametrize("g", [(-1,), (1,)], ids=str)
+def test_conv1d_direct(g):
+    s, x, f, b = random_conv_case(103, 1, g, 3, 4, 5, 40, 5)
+    assert_parity(gpu_conv(g, x, f, b), oracle.conv_nd(x, f, b, g))
+
+
+@pytest.mark.parametrize("g", [(0,), (0, 0), (0, 0, 0)], ids=str)
+def test_all_zero_signature_rejected(g):
+    s, x, f, b = random_conv_case(113, len(g), (1,) * len(g), 1, 2, 2, 5, 3)
+    gpu_conv(g, x, f, b, expect=P.CLIFF_EINVAL)
+
+
+def test_mfma_covers_main_2d_and_3d_shapes():
+    # the matrix-core path must accept the benchmark-like shapes
+    for g, shape in (((1, 1), (1, 8, 64, 20, 3)), ((1, 1, 1), (1, 4, 32, 8, 3))):
+        s, x, f, b = _case(104, g, shape)
+        y = gpu_conv(g, x, f, b, algo=P.ALGO_MFMA)
+        assert_parity(y, oracle.conv_nd(x, f, b, g))
+
+
+def test_no_bias():
+    g = (1, -1)
+    s, x, f, b = _case(105, g, (2, 3, 8, 10, 3))
+    assert_parity(gpu_conv(g, x, f, None), oracle.conv_nd(x, f, None, g))
+
+
+ACTS = [(AGG_LINEAR, (0, 1, 2, 3)), (AGG_SUM, (0, 1, 2, 3)), (AGG_MEAN, (0, 1, 2, 3)),
+        (AGG_LINEAR, (2,)), (AGG_MEAN, (3, 0)), (AGG_SUM, (1, 3, 2))]
+
+
+def _act_args(seed, C, mode, blades):
+    rng = np.random.default_rng(seed)
+    aw = rng.standard_normal((C, len(blades))).astype(np.float32) if mode == AGG_LINEAR else None
+    ab = (0.1 * rng.standard_normal(C)).astype(np.float32) if mode == AGG_LINEAR else None
+    return aw, ab
+
+
+@pytest.mark.parametrize("algo", [P.ALGO_MFMA, P.ALGO_DIRECT], ids=["mfma", "direct"])
+@pytest.mark.parametrize("mode,blades", ACTS, ids=str)
+def test_fused_act_2d(algo, mode, blades):
+    g = (1, -1)
+    s, x, f, b = _case(106, g, (3, 5, 70, 12, 3))
+    aw, ab = _act_args(5, 70, mode, blades)
+    y = gpu_conv(g, x, f, b, act=(mode, blades, aw, ab), algo=algo)
+    ref = oracle.act(oracle.conv_nd(x, f, b, g), mode, blades, aw, ab)
+    assert_parity(y, ref)
+
+
+ACTS3 = [(AGG_MEAN, tuple(range(8))), (AGG_LINEAR, tuple(range(8))),
+         (AGG_SUM, (7, 0, 4)), (AGG_LINEAR, (3, 5)), (AGG_MEAN, (6,))]
+
+
+@pytest.mark.parametrize("algo", [P.ALGO_MFMA, P.ALGO_DIRECT], ids=["mfma", "direct"])
+@pytest.mark.parametrize("mode,blades", ACTS3, ids=str)
+def test_fused_act_3d(algo, mode, blades):
+    g = (1, 1, 1)
+    s, x, f, b = _case(107, g, (2, 3, 33, 8, 3))
+    aw, ab = _act_args(6, 33, mode, blades)
+    y = gpu_conv(g, x, f, b, act=(mode, blades, aw, ab), algo=algo)
+    ref = oracle.act(oracle.conv_nd(x, f, b, g), mode, blades, aw, ab)
+    assert_parity(y, ref)
+
+
+def test_fused_equals_unfused_act():
+    g = (1, 1, 1)
+    s, x, f, b = _case(108, g, (2, 4, 32, 10, 3))
+    mode, blades = AGG_LINEAR, tuple(range(8))
+    aw, ab = _act_args(7, 32, mode, blades)
+    fused = gpu_conv(g, x, f, b, act=(mode, blades, aw, ab))
+    plain = gpu_conv(g, x, f, b)
+    unfused = gpu_act(plain, mode, blades, aw, ab)
+    assert normwise(fused, unfused) <= 1e-6
+
+
+def test_deterministic():
+    g = (1, 1)
+    s, x, f, b = _case(109, g, (3, 6, 64, 20, 3))
+    xt, ft, bt = dev(x), dev(f), dev(b)
+    y1 = gpu_conv(g, x, f, b, xt=xt, ft=ft, bt=bt)
+    y2 = gpu_conv(g, x, f, b, xt=xt, ft=ft, bt=bt)
+    np.testing.assert_array_equal(y1, y2)
+
+
+@pytest.mark.parametrize("nb", [2, 4, 8])
+@pytest.mark.parametrize("mode", [AGG_LINEAR, AGG_SUM, AGG_MEAN])
+def test_standalone_act(nb, mode):
+    K = max(1, nb - 1)
+    x, spec, aw, ab = random_act_case(200 + nb, nb, 3, 7, 11, mode, K)
+    y = gpu_act(x, mode, spec.blades, aw, ab)
+    assert_parity(y, oracle.act(x, mode, spec.blades, aw, ab))
+
+
+def test_standalone_act_inplace_and_p1():
+    x, spec, aw, ab = random_act_case(210, 8, 5, 9, 1, AGG_LINEAR, 8)
+    y = gpu_act(x, AGG_LINEAR, spec.blades, aw, ab, inplace=True)
+    assert_parity(y, oracle.act(x, AGG_LINEAR, spec.blades, aw, ab))
+
+
+def test_zero_batch_is_noop():
+    g = (1, 1)
+    s, x, f, b = _case(111, g, (1, 2, 3, 6, 3))
+    xt, ft = dev(x), dev(f)
+    out = dev(np.zeros((1, 3, 4, 4, 4), np.float32))
+    st = P.clifford_conv_nd(2, g, 0, 2, 3, 6, 3, xt.data_ptr(), ft.data_ptr(), 0,
+                            out.data_ptr())
+    assert st == P.CLIFF_OK
+    assert float(out.abs().sum()) == 0.0
+
+
+def test_errors_with_real_buffers():
+    g = (1, 1)
+    s, x, f, b = _case(112, g, (2, 3, 4, 8, 3))
+    xt, ft, bt = dev(x), dev(f), dev(b)
+    out = dev(np.zeros(s.output_shape(), np.float32))
+    args = [2, g, 2, 3, 4, 8, 3]
+    # misaligned output (4-byte offset), output overlapping the input
+    assert P.clifford_conv_nd(*args, xt.data_ptr(), ft.data_ptr(), bt.data_ptr(),
+                              out.data_ptr() + 4) == P.CLIFF_EALIGN
+    assert P.clifford_conv_nd(*args, xt.data_ptr(), ft.data_ptr(), bt.data_ptr(),
+                              xt.data_ptr()) == P.CLIFF_EOVERLAP
+    # untouched output after an error
+    assert float(out.abs().sum()) == 0.0
