@@ -55,8 +55,9 @@ struct MfmaArgs {
     ActParams act;
 };
 
-template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS>
-__global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
+template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS,
+          int WAVES_PER_SIMD>
+__global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_kernel(MfmaArgs a)
 {
     constexpr int NT = 64 * WCO * WPOS;
     constexpr int CPT = 16 / NB;  // output channels per 16-row tile
@@ -100,22 +101,32 @@ __global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
     const int n_rows = pl0 == pl1 ? len0
                                   : len0 + (pl1 - pl0 - 1) * D + (r1 - pl1 * Do) + df;
 
-    // Staging slots of this thread (fixed for all stages).
+    // Staging.  A stage buffer holds float4 slots in staging order: the slab
+    // rows [0, slab_f4), then the filters [co][tap][blade] [slab_f4, total_f4).
+    // Slot t of this lane is buffer float4 f = t * NT + tid, so each wave
+    // fills 64 consecutive float4 per slot with one direct global->LDS load
+    // (global_load_lds_dwordx4: lane i lands at the wave's LDS base + 16 i).
+    // goff >= 0: input float offset from the stage's slab base; goff < 0:
+    // -1 - filter float offset from the stage's filter base (channels past
+    // C_out read the last channel; their results are never stored).
     const int slab_f4 = n_rows * row_f4;
     const int wq_f4 = taps2 * NB / 4;
     const int total_f4 = slab_f4 + CO_WG * wq_f4;
-    int64_t goff[SLOTS];
-    int ldst[SLOTS];
-    int kind[SLOTS];  // 0 input, 1 filter, 2 zero filter (co >= C_out), 3 idle
+    const int w_lds = slab_f4 * 4;  // float offset of the filters in a buffer
+    const int b0 = KD == 2 ? pl0 : pl0 / Do;
+    const int z0 = KD == 2 ? 0 : pl0 - b0 * Do;
+    const int plane_floats = D * row_floats;  // one d_image x d_image plane
+    int goff[SLOTS];
 #pragma unroll
     for (int t = 0; t < SLOTS; ++t) {
-        const int f = tid + t * NT;
+        const int f = t * NT + tid;
         goff[t] = 0;
-        ldst[t] = 0;
-        kind[t] = 3;
         if (f < slab_f4) {
             const int row = f / row_f4;
-            const int col = f - row * row_f4;
+            const int sr = f - row * row_f4;
+            // N_B = 8 rows are stored [half][x][4]: slot sr = half * D + x
+            // holds the global float4 2 x + half of the row
+            const int col = NB == 8 ? 2 * (sr % D) + sr / D : sr;
             int pl, yin;
             if (row < len0) {
                 pl = pl0;
@@ -125,54 +136,46 @@ __global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
                 pl = pl0 + 1 + s2 / D;
                 yin = s2 - (s2 / D) * D;
             }
-            int64_t base;
+            int rel;  // planes between pl0's first row and this row's plane
             if (KD == 2) {
-                base = ((int64_t)pl * a.C_in * D + yin) * row_floats;
+                rel = (pl - pl0) * a.C_in;
             } else {
                 const int b = pl / Do, z = pl - (pl / Do) * Do;
-                base = (((int64_t)b * a.C_in * D + z) * D + yin) * row_floats;
+                rel = ((b - b0) * a.C_in * D + (z - z0));
             }
-            goff[t] = base + col * 4;
-            ldst[t] = row * row_floats +
-                      (NB == 8 ? (col & 1) * D * 4 + (col >> 1) * 4 : col * 4);
-            kind[t] = 0;
+            goff[t] = rel * plane_floats + yin * row_floats + col * 4;
         } else if (f < total_f4) {
             const int e = f - slab_f4;
             const int co_l = e / wq_f4;
             const int r4 = e - co_l * wq_f4;
-            const int co = co0 + co_l;
-            goff[t] = (int64_t)co * taps_full * NB + r4 * 4;
-            ldst[t] = a.slab_floats + co_l * taps2 * NB + r4 * 4;
-            kind[t] = co < a.C_out ? 1 : 2;
+            const int co = min(co0 + co_l, a.C_out - 1);
+            goff[t] = -1 - ((co - co0) * taps_full * NB + r4 * 4);
         }
     }
 
-    const int64_t x_cstride = (int64_t)D * D * (KD == 3 ? D : 1) * NB;
+    const int64_t x_cstride = (int64_t)plane_floats * (KD == 3 ? D : 1);
     const int64_t w_cstride = (int64_t)a.C_out * taps_full * NB;
-    f4 stg[SLOTS];
-    auto load_stage = [&](int s) {
+    const float* xbase = a.x + ((int64_t)b0 * a.C_in * (KD == 3 ? D : 1) + z0) * plane_floats;
+    const float* wbase = a.w + (int64_t)co0 * taps_full * NB;
+    const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
+    auto load_stage = [&](int s, int buf) {
         int ci = s, qz = 0;
         if (KD == 3) {
             ci = s / df;
             qz = s - ci * df;
         }
-        const int64_t xs = ci * x_cstride + (int64_t)qz * D * D * NB;
-        const int64_t ws = ci * w_cstride + (int64_t)qz * taps2 * NB;
+        const float* xs = xbase + ci * x_cstride + (int64_t)qz * plane_floats;
+        const float* ws = wbase + ci * w_cstride + (int64_t)qz * taps2 * NB;
+        float* lbase = smem + buf * a.stage_floats + wave_u * 256;
 #pragma unroll
         for (int t = 0; t < SLOTS; ++t) {
-            if (kind[t] == 0)
-                stg[t] = *reinterpret_cast<const f4*>(a.x + goff[t] + xs);
-            else if (kind[t] == 1)
-                stg[t] = *reinterpret_cast<const f4*>(a.w + goff[t] + ws);
-            else
-                stg[t] = f4{0.f, 0.f, 0.f, 0.f};
+            if (t * NT + tid < total_f4) {
+                const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
+                __builtin_amdgcn_global_load_lds(
+                    src, (__attribute__((address_space(3))) void*)(lbase + t * NT * 4), 16, 0,
+                    0);
+            }
         }
-    };
-    auto store_stage = [&](int buf) {
-        float* base = smem + buf * a.stage_floats;
-#pragma unroll
-        for (int t = 0; t < SLOTS; ++t)
-            if (kind[t] != 3) *reinterpret_cast<f4*>(base + ldst[t]) = stg[t];
     };
 
     // Per-lane constants of the MFMA fragments.
@@ -193,7 +196,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
     for (int h = 0; h < NH; ++h) {
         const int j = 4 * h + kk;
         sg[h] = sign_of(a.sign, i_a * NB + j);
-        wofs[h] = a.slab_floats + (wco * MW * CPT + co_a) * taps2 * NB +
+        wofs[h] = w_lds + (wco * MW * CPT + co_a) * taps2 * NB +
                   src_blade(NB, i_a, j);
     }
     // B: row kk = input blade, column mrow = output position.
@@ -253,14 +256,14 @@ __global__ __launch_bounds__(64 * WCO * WPOS) void conv_mfma_kernel(MfmaArgs a)
 
     // Main loop: one barrier per stage; the next stage's global loads are in
     // flight while the current one is multiplied.
-    load_stage(0);
-    store_stage(0);
+    load_stage(0, 0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     for (int s = 0; s < a.n_stage; ++s) {
-        const bool more = s + 1 < a.n_stage;
-        if (more) load_stage(s + 1);
+        // buffer (s+1)&1 was last read in iteration s-1, before the barrier
+        if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
         compute(s & 1);
-        if (more) store_stage((s + 1) & 1);
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
 
@@ -310,10 +313,9 @@ struct TileCfg {
     int wco, wpos, mw, nw;
 };
 
-template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW>
+template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
 cliff_status run(const ConvProblem& p, hipStream_t stream)
 {
-    constexpr int SLOTS = 8;
     constexpr int NT = 64 * WCO * WPOS;
     constexpr int CPT = 16 / NB;
     constexpr int CO_WG = WCO * MW * CPT;
@@ -338,6 +340,10 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     const int64_t lds_bytes = 2 * stage_floats * 4;
     if (lds_bytes > 64 * 1024) return CLIFF_EUNSUPPORTED;
     if ((slab_floats + w_floats) / 4 > (int64_t)SLOTS * NT) return CLIFF_EUNSUPPORTED;
+    // staging offsets are 32-bit, relative to the block's first plane
+    int64_t img = NB;
+    for (int t = 0; t < KD; ++t) img *= D;
+    if ((planes + 2) * p.C_in * img >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
 
     MfmaArgs a;
     a.x = p.x;
@@ -358,7 +364,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     a.stage_floats = (int)stage_floats;
     a.sign = p.sign;
     a.act = p.act;
-    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS>),
+    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS, WAVES>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
@@ -370,10 +376,10 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
     // narrow: few channels, 256 positions (small C_out).
     constexpr int CO_WIDE = 2 * 8 * (16 / NB);
     if (p.C_out * 2 > CO_WIDE) {
-        const cliff_status s = run<KD, NB, DF, 2, 2, 8, 4>(p, stream);
+        const cliff_status s = run<KD, NB, DF, 2, 2, 8, 4, 6, 2>(p, stream);
         if (s != CLIFF_EUNSUPPORTED) return s;
     }
-    return run<KD, NB, DF, 1, 4, 2, 4>(p, stream);
+    return run<KD, NB, DF, 1, 4, 2, 4, 8, 2>(p, stream);
 }
 
 }  // namespace
