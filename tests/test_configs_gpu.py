@@ -64,14 +64,14 @@ def _sample_points(shape: W.ConvShape, n_random: int, seed: int):
 
 
 def test_c1_full():
-    w = W.WORKLOADS["c1_2d_tiny"]
+    w = W.WORKLOADS["conv2d_c4_d16"]
     x, ps = W.make_inputs(w)
     y = _gpu_block(w, x, ps)
     ref = oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g)
     assert_parity(y, ref)
 
 
-@pytest.mark.parametrize("name", ["c2_2d_c64_d128", "c3_3d_c32_d32"])
+@pytest.mark.parametrize("name", ["conv2d_c64_d128", "conv3d_c32_d32"])
 def test_single_conv_sampled(name):
     w = W.WORKLOADS[name]
     x, ps = W.make_inputs(w)
@@ -93,8 +93,8 @@ def _patch_origins(d_final, ps, k, seed):
     return origins
 
 
-@pytest.mark.parametrize("name,ps", [("c4_2d_block_c64_d130", 12),
-                                     ("c5_3d_block_c64_d36", 4)])
+@pytest.mark.parametrize("name,ps", [("block2d_c64_d130", 12),
+                                     ("block3d_c64_d36", 4)])
 def test_block_patches(name, ps):
     w = W.WORKLOADS[name]
     x, params = W.make_inputs(w)

@@ -114,25 +114,25 @@ def _fan_bound(C_in, d_filter, k):
 
 # The five workloads the benchmark and the full-size parity tests use.
 WORKLOADS = {
-    "c1_2d_tiny": Workload(
-        "c1_2d_tiny", 1000,
+    "conv2d_c4_d16": Workload(
+        "conv2d_c4_d16", 1000,
         _conv_layers(2, (1, 1), 8, 4, 16, 3, 1), (None,),
         (_fan_bound(4, 3, 2),), bias_std=1.0),
-    "c2_2d_c64_d128": Workload(
-        "c2_2d_c64_d128", 1001,
+    "conv2d_c64_d128": Workload(
+        "conv2d_c64_d128", 1001,
         _conv_layers(2, (1, 1), 8, 64, 128, 3, 1), (None,),
         (_fan_bound(64, 3, 2),), bias_std=0.1),
-    "c3_3d_c32_d32": Workload(
-        "c3_3d_c32_d32", 1002,
+    "conv3d_c32_d32": Workload(
+        "conv3d_c32_d32", 1002,
         _conv_layers(3, (1, 1, 1), 8, 32, 32, 3, 1), (None,),
         (_fan_bound(32, 3, 3),), bias_std=0.1),
-    "c4_2d_block_c64_d130": Workload(
-        "c4_2d_block_c64_d130", 1003,
+    "block2d_c64_d130": Workload(
+        "block2d_c64_d130", 1003,
         _conv_layers(2, (1, -1), 8, 64, 130, 3, 2),
         (ActSpec(AGG_LINEAR, (0, 1, 2, 3)), ActSpec(AGG_LINEAR, (0, 1, 2, 3))),
         (_fan_bound(64, 3, 2),) * 2, bias_std=0.1),
-    "c5_3d_block_c64_d36": Workload(
-        "c5_3d_block_c64_d36", 1004,
+    "block3d_c64_d36": Workload(
+        "block3d_c64_d36", 1004,
         _conv_layers(3, (1, 1, 1), 8, 64, 36, 3, 2),
         (ActSpec(AGG_MEAN, tuple(range(8))), ActSpec(AGG_MEAN, tuple(range(8)))),
         (_fan_bound(64, 3, 3),) * 2, bias_std=0.1),
