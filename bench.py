@@ -34,6 +34,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3   # 256 CU x 2.4 GHz x 256 FLOP/clk/CU
 PEAK_HBM_GBS = 8000.0
 HEADLINE = "conv2d_c64_d128"
 KERNEL_SOURCES = ["paper_2507_01040_amd/csrc/conv_mfma.hip",
+                  "paper_2507_01040_amd/build.py",
                   "paper_2507_01040_amd/csrc/common.hpp",
                   "paper_2507_01040_amd/csrc/epilogue.hpp"]
 

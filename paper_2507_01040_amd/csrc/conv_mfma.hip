@@ -222,6 +222,9 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
     const int wtile = CPT * taps2 * NB;  // LDS floats between channel tiles
     auto compute = [&](int buf) {
         const float* S = smem + buf * a.stage_floats;
+#if defined(CLIFF_SCHED)
+        __builtin_amdgcn_iglp_opt(CLIFF_SCHED);
+#endif
 #pragma unroll
         for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
             for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
@@ -369,17 +372,35 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
 
-template <int KD, int NB, int DF>
-cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
+// Wide tile (workgroup = WCO x WPOS waves, each MW x NW MFMA tiles).
+// Chosen by measurement on MI355X: k = 2 takes all 64 channels of the 2D
+// workloads in one workgroup (4 x 1 waves of 4 x 8 tiles, 2 waves/SIMD); k = 3
+// does best with smaller 4 x 4 tiles at 3 waves/SIMD.
+#ifndef CLIFF_W2
+#define CLIFF_W2 4, 1, 4, 8, 6, 2  // WCO, WPOS, MW, NW, SLOTS, waves/SIMD (k = 2)
+#endif
+#ifndef CLIFF_W3
+#define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
+#endif
+
+template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
+cliff_status run_wide_or_narrow(const ConvProblem& p, hipStream_t stream)
 {
-    // wide: all (or half) of the output channels per workgroup, 128 positions;
+    // wide: all (or half) of the output channels per workgroup;
     // narrow: few channels, 256 positions (small C_out).
-    constexpr int CO_WIDE = 2 * 8 * (16 / NB);
+    constexpr int CO_WIDE = WCO * MW * (16 / NB);
     if (p.C_out * 2 > CO_WIDE) {
-        const cliff_status s = run<KD, NB, DF, 2, 2, 8, 4, 6, 2>(p, stream);
+        const cliff_status s = run<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS, WAVES>(p, stream);
         if (s != CLIFF_EUNSUPPORTED) return s;
     }
     return run<KD, NB, DF, 1, 4, 2, 4, 8, 2>(p, stream);
+}
+
+template <int KD, int NB, int DF>
+cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
+{
+    if (KD == 2) return run_wide_or_narrow<KD, NB, DF, CLIFF_W2>(p, stream);
+    return run_wide_or_narrow<KD, NB, DF, CLIFF_W3>(p, stream);
 }
 
 }  // namespace
