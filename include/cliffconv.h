@@ -114,15 +114,22 @@ cliff_status clifford_conv_nd(int k, const int8_t* g, int64_t B, int64_t C_in,
 
 /* Kernel choice for clifford_conv_nd_algo. */
 typedef enum {
-    CLIFF_ALGO_AUTO = 0,   /* what clifford_conv_nd does */
-    CLIFF_ALGO_DIRECT = 1, /* one thread per output multivector, fp32 FMA */
-    CLIFF_ALGO_MFMA = 2    /* implicit GEMM on fp32 MFMA (k = 2, 3 only) */
+    CLIFF_ALGO_AUTO = 0,        /* what clifford_conv_nd does */
+    CLIFF_ALGO_DIRECT = 1,      /* one thread per output multivector, fp32 FMA */
+    CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA (k = 2, 3 only),
+                                   tile shape chosen from the problem size */
+    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=2) / 16 (k=3)
+                                   channels x 128 positions per workgroup */
+    CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 32 channels x 32 positions */
+    CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 4 channels x 256 positions */
+    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 4 / 2 channels x 32 positions, one wave */
 } cliff_algo;
 
 /*
  * Same operation and contract as clifford_conv_nd, with the kernel family
- * forced (CLIFF_EUNSUPPORTED if that family cannot run the request).  For
- * tests and benchmarks that compare the two families.
+ * (and for the MFMA family optionally the tile shape) forced;
+ * CLIFF_EUNSUPPORTED if that choice cannot run the request.  For tests and
+ * benchmarks that compare kernels.
  */
 cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
                                    int64_t C_in, int64_t C_out, int64_t d_image,

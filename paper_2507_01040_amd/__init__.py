@@ -24,6 +24,7 @@ STATUS_NAMES = {0: "CLIFF_OK", 1: "CLIFF_EINVAL", 2: "CLIFF_ESHAPE",
                 5: "CLIFF_EUNSUPPORTED", 6: "CLIFF_EDEVICE"}
 AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
 ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
+ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
 
 EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "multivector_act",
             "cliffconv_cayley_table", "cliffconv_status_string")

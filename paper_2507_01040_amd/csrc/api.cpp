@@ -141,7 +141,7 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
 {
     if (!g || !input || !filters || !output) return CLIFF_EINVAL;
     if (!valid_k(k) || !valid_signature(k, g)) return CLIFF_EINVAL;
-    if (algo < CLIFF_ALGO_AUTO || algo > CLIFF_ALGO_MFMA) return CLIFF_EINVAL;
+    if (algo < CLIFF_ALGO_AUTO || algo > CLIFF_ALGO_MFMA_TINY) return CLIFF_EINVAL;
     const int nb = 1 << k;
     bool linear = false;
     if (act) {
@@ -165,7 +165,8 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
         (linear && (overlaps(output, out_bytes, act->weight, C_out * act->K * 4) ||
                     overlaps(output, out_bytes, act->bias, C_out * 4))))
         return CLIFF_EOVERLAP;
-    if (algo == CLIFF_ALGO_MFMA && k == 1) return CLIFF_EUNSUPPORTED;
+    const bool mfma_forced = algo >= CLIFF_ALGO_MFMA;
+    if (mfma_forced && k == 1) return CLIFF_EUNSUPPORTED;
     if (B == 0) return CLIFF_OK;
 
     int8_t src[64], sign[64];
@@ -185,12 +186,13 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
     p.y = output;
     p.sign = pack_signs(nb, sign);
     p.act = to_params(act);
+    p.mfma_shape = algo >= CLIFF_ALGO_MFMA_WIDE ? algo - CLIFF_ALGO_MFMA_WIDE : -1;
     hipStream_t st = (hipStream_t)stream;
 
     if (algo == CLIFF_ALGO_DIRECT) return launch_conv_direct(p, st);
     if (k >= 2) {
         const cliff_status s = launch_conv_mfma(p, st);
-        if (s != CLIFF_EUNSUPPORTED || algo == CLIFF_ALGO_MFMA) return s;
+        if (s != CLIFF_EUNSUPPORTED || mfma_forced) return s;
     }
     return launch_conv_direct(p, st);
 }

@@ -54,6 +54,7 @@ struct ConvProblem {
     float* y;
     SignMasks sign;
     ActParams act;
+    int mfma_shape;  // -1: chosen from the problem; 0..3: wide, medium, narrow, tiny
 };
 
 // host-side launchers (defined in the .hip files)

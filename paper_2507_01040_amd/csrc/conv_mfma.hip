@@ -21,15 +21,17 @@
 // Work decomposition.  The flattened output positions m in [0, B d_out^k)
 // are cut into blocks of P consecutive positions (they may span rows, planes
 // and batch entries); a workgroup computes P positions x CO_WG output
-// channels.  The K loop runs over "stages": one input channel (2D) or one
-// (input channel, filter plane qz) pair (3D).  For each stage the workgroup
-// stages in LDS (double-buffered through registers):
+// channels.  The K loop runs over "stages": cc input channels (2D) or cc
+// input channels of one filter plane qz (3D); the host picks cc so a stage
+// holds enough MFMAs per barrier.  For each stage and channel the workgroup
+// stages in LDS (double-buffered, direct global->LDS loads):
 //   * the slab: every input row the block's outputs touch for this stage,
 //     rows of d_image multivectors, kept blade-packed ([row][x][4] for N_B = 4,
 //     [row][half][x][4] for N_B = 8 so that a fragment read is 64 consecutive
 //     words);
 //   * the raw filters [co][tap][blade] of this stage (no expansion).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "epilogue.hpp"
@@ -47,15 +49,15 @@ struct MfmaArgs {
     int C_in, C_out, D, Do, df;
     int M;          // number of output positions B * d_out^k
     int npos;       // d_out^k
-    int n_stage;    // C_in (k = 2) or C_in * d_filter (k = 3)
+    int cc;         // input channels per stage
+    int n_stage;    // ceil(C_in / cc) (k = 2) or that times d_filter (k = 3)
     int n_co_blk, n_blk;
-    int slab_floats;   // LDS floats reserved for the slab in one buffer
-    int stage_floats;  // slab + filters, one buffer
+    int stage_floats;  // LDS floats of one stage buffer
     SignMasks sign;
     ActParams act;
 };
 
-template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS,
+template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
           int WAVES_PER_SIMD>
 __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_kernel(MfmaArgs a)
 {
@@ -101,29 +103,38 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
     const int n_rows = pl0 == pl1 ? len0
                                   : len0 + (pl1 - pl0 - 1) * D + (r1 - pl1 * Do) + df;
 
-    // Staging.  A stage buffer holds float4 slots in staging order: the slab
-    // rows [0, slab_f4), then the filters [co][tap][blade] [slab_f4, total_f4).
-    // Slot t of this lane is buffer float4 f = t * NT + tid, so each wave
-    // fills 64 consecutive float4 per slot with one direct global->LDS load
-    // (global_load_lds_dwordx4: lane i lands at the wave's LDS base + 16 i).
-    // goff >= 0: input float offset from the stage's slab base; goff < 0:
-    // -1 - filter float offset from the stage's filter base (channels past
-    // C_out read the last channel; their results are never stored).
-    const int slab_f4 = n_rows * row_f4;
+    // Staging.  A stage buffer holds float4 slots in staging order: cc
+    // channel slabs [cc][slab rows] in [0, cc * slab_f4), then cc channels of
+    // filters [cc][co][tap][blade].  Slot t of this lane is buffer float4
+    // f = t * NT + tid, so each wave fills 64 consecutive float4 per slot with
+    // one direct global->LDS load (global_load_lds_dwordx4: lane i lands at
+    // the wave's LDS base + 16 i).  goff >= 0: input float offset from the
+    // stage's slab base; goff < 0: -1 - filter float offset from the stage's
+    // filter base (channels past C_out read the last channel; their results
+    // are never stored).  Slots are channel-major within each section, so a
+    // stage with nv < cc valid channels loads f < nv * slab_f4 (slab) and
+    // f - cc * slab_f4 < nv * wch_f4 (filters).
+    const int cc = CCT > 0 ? CCT : a.cc;  // CCT > 0: channels per stage fixed
+    const int slab_f4 = n_rows * row_f4;  // one channel's slab
     const int wq_f4 = taps2 * NB / 4;
-    const int total_f4 = slab_f4 + CO_WG * wq_f4;
-    const int w_lds = slab_f4 * 4;  // float offset of the filters in a buffer
+    const int wch_f4 = CO_WG * wq_f4;     // one channel's filters
+    const int total_f4 = cc * (slab_f4 + wch_f4);
+    const int w_lds = cc * slab_f4 * 4;   // float offset of the filters in a buffer
     const int b0 = KD == 2 ? pl0 : pl0 / Do;
     const int z0 = KD == 2 ? 0 : pl0 - b0 * Do;
     const int plane_floats = D * row_floats;  // one d_image x d_image plane
+    const int x_cstride = plane_floats * (KD == 3 ? D : 1);  // < 2^31 (host check)
+    const int w_cstride = a.C_out * taps_full * NB;
     int goff[SLOTS];
 #pragma unroll
     for (int t = 0; t < SLOTS; ++t) {
         const int f = t * NT + tid;
         goff[t] = 0;
-        if (f < slab_f4) {
-            const int row = f / row_f4;
-            const int sr = f - row * row_f4;
+        if (f < cc * slab_f4) {
+            const int c_l = f / slab_f4;
+            const int fr = f - c_l * slab_f4;
+            const int row = fr / row_f4;
+            const int sr = fr - row * row_f4;
             // N_B = 8 rows are stored [half][x][4]: slot sr = half * D + x
             // holds the global float4 2 x + half of the row
             const int col = NB == 8 ? 2 * (sr % D) + sr / D : sr;
@@ -143,33 +154,47 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                 const int b = pl / Do, z = pl - (pl / Do) * Do;
                 rel = ((b - b0) * a.C_in * D + (z - z0));
             }
-            goff[t] = rel * plane_floats + yin * row_floats + col * 4;
+            goff[t] = c_l * x_cstride + rel * plane_floats + yin * row_floats + col * 4;
         } else if (f < total_f4) {
-            const int e = f - slab_f4;
-            const int co_l = e / wq_f4;
-            const int r4 = e - co_l * wq_f4;
+            const int e = f - cc * slab_f4;
+            const int c_l = e / wch_f4;
+            const int e2 = e - c_l * wch_f4;
+            const int co_l = e2 / wq_f4;
+            const int r4 = e2 - co_l * wq_f4;
             const int co = min(co0 + co_l, a.C_out - 1);
-            goff[t] = -1 - ((co - co0) * taps_full * NB + r4 * 4);
+            goff[t] = -1 - (c_l * w_cstride + (co - co0) * taps_full * NB + r4 * 4);
         }
     }
 
-    const int64_t x_cstride = (int64_t)plane_floats * (KD == 3 ? D : 1);
-    const int64_t w_cstride = (int64_t)a.C_out * taps_full * NB;
     const float* xbase = a.x + ((int64_t)b0 * a.C_in * (KD == 3 ? D : 1) + z0) * plane_floats;
     const float* wbase = a.w + (int64_t)co0 * taps_full * NB;
     const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
-    auto load_stage = [&](int s, int buf) {
-        int ci = s, qz = 0;
+    // channels of stage s: [ci0, ci0 + n_valid), filter plane qz
+    auto stage_channels = [&](int s, int& ci0, int& qz) {
+        int cg = s;
+        qz = 0;
         if (KD == 3) {
-            ci = s / df;
-            qz = s - ci * df;
+            cg = s / df;
+            qz = s - cg * df;
         }
-        const float* xs = xbase + ci * x_cstride + (int64_t)qz * plane_floats;
-        const float* ws = wbase + ci * w_cstride + (int64_t)qz * taps2 * NB;
+        ci0 = cg * cc;
+        return min(cc, a.C_in - ci0);
+    };
+    auto load_stage = [&](int s, int buf) {
+        int ci0, qz;
+        const int nv = stage_channels(s, ci0, qz);
+        const float* xs = xbase + (int64_t)ci0 * x_cstride + (int64_t)qz * plane_floats;
+        const float* ws = wbase + (int64_t)ci0 * w_cstride + (int64_t)qz * taps2 * NB;
         float* lbase = smem + buf * a.stage_floats + wave_u * 256;
 #pragma unroll
         for (int t = 0; t < SLOTS; ++t) {
-            if (t * NT + tid < total_f4) {
+            const int f = t * NT + tid;
+            // with one channel per stage every stage is full
+            const bool load = CCT == 1 ? f < total_f4
+                                       : (goff[t] >= 0 ? f < nv * slab_f4
+                                                       : (f < total_f4 &&
+                                                          f - cc * slab_f4 < nv * wch_f4));
+            if (load) {
                 const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
                 __builtin_amdgcn_global_load_lds(
                     src, (__attribute__((address_space(3))) void*)(lbase + t * NT * 4), 16, 0,
@@ -220,11 +245,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
         for (int nw = 0; nw < NW; ++nw) acc[mw][nw] = f4{0.f, 0.f, 0.f, 0.f};
 
     const int wtile = CPT * taps2 * NB;  // LDS floats between channel tiles
-    auto compute = [&](int buf) {
-        const float* S = smem + buf * a.stage_floats;
-#if defined(CLIFF_SCHED)
-        __builtin_amdgcn_iglp_opt(CLIFF_SCHED);
-#endif
+    auto compute = [&](int buf, int nv) {
+      for (int c_l = 0; c_l < (CCT > 0 ? CCT : nv); ++c_l) {
+        // B fragments index S from the channel's slab, A fragments from the
+        // channel's filters (wofs already includes the filter offset)
+        const float* S = smem + buf * a.stage_floats + c_l * slab_f4 * 4;
+        const float* Sw = smem + buf * a.stage_floats + c_l * wch_f4 * 4;
 #pragma unroll
         for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
             for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
@@ -239,7 +265,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                             float av[MW], bv[NW];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
-                                av[mw] = S[wofs[h] + mw * wtile + tap * NB] * sg[h];
+                                av[mw] = Sw[wofs[h] + mw * wtile + tap * NB] * sg[h];
 #pragma unroll
                             for (int nw = 0; nw < NW; ++nw)
                                 bv[nw] = S[xoff[nw] + qy_ * row_floats + h * D * 4 +
@@ -255,6 +281,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                 }
             }
         }
+      }
     };
 
     // Main loop: one barrier per stage; the next stage's global loads are in
@@ -265,7 +292,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
     for (int s = 0; s < a.n_stage; ++s) {
         // buffer (s+1)&1 was last read in iteration s-1, before the barrier
         if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
-        compute(s & 1);
+        int ci0, qz;
+        compute(s & 1, stage_channels(s, ci0, qz));
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
@@ -316,7 +344,8 @@ struct TileCfg {
     int wco, wpos, mw, nw;
 };
 
-template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
+template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
+          int WAVES>
 cliff_status run(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NT = 64 * WCO * WPOS;
@@ -337,16 +366,25 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     const int64_t R = std::min<int64_t>((P - 1) / Do + 2, total_rows);
     const int64_t planes = std::min<int64_t>(R, (R - 1) / Do + 2);
     const int64_t rows_max = R + planes * (df - 1);
-    const int64_t slab_floats = rows_max * D * NB;
-    const int64_t w_floats = CO_WG * df * df * NB;
-    const int64_t stage_floats = slab_floats + w_floats;
+    const int64_t ch_floats = rows_max * D * NB + CO_WG * df * df * NB;  // per channel
+    // Channels per stage: enough MFMAs per wave between barriers, within the
+    // LDS budget (two buffers) and the staging slots.
+    constexpr int64_t LDS_BUDGET = 64 * 1024;
+    constexpr int64_t MFMA_PER_STAGE = 512;
+    const int64_t mfma_per_ch = df * df * (NB / 4) * MW * NW;
+    int64_t cc = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
+    cc = std::min<int64_t>(cc, LDS_BUDGET / (2 * ch_floats * 4));
+    cc = std::min<int64_t>(cc, (int64_t)SLOTS * NT / (ch_floats / 4));
+    if (CCT > 0) cc = cc >= CCT ? CCT : 0;
+    if (cc < 1) return CLIFF_EUNSUPPORTED;
+    const int64_t stage_floats = cc * ch_floats;
     const int64_t lds_bytes = 2 * stage_floats * 4;
-    if (lds_bytes > 64 * 1024) return CLIFF_EUNSUPPORTED;
-    if ((slab_floats + w_floats) / 4 > (int64_t)SLOTS * NT) return CLIFF_EUNSUPPORTED;
     // staging offsets are 32-bit, relative to the block's first plane
     int64_t img = NB;
     for (int t = 0; t < KD; ++t) img *= D;
-    if ((planes + 2) * p.C_in * img >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
+    if ((cc + (planes + 2) * p.C_in) * img >= (1ll << 31) ||
+        cc * p.C_out * df * df * (KD == 3 ? df : 1) * NB >= (1ll << 31))
+        return CLIFF_EUNSUPPORTED;
 
     MfmaArgs a;
     a.x = p.x;
@@ -360,47 +398,114 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     a.df = (int)df;
     a.M = (int)M;
     a.npos = (int)npos;
-    a.n_stage = (int)(KD == 2 ? p.C_in : p.C_in * df);
+    a.cc = (int)cc;
+    const int64_t n_cgrp = (p.C_in + cc - 1) / cc;
+    a.n_stage = (int)(KD == 2 ? n_cgrp : n_cgrp * df);
     a.n_co_blk = (int)n_co_blk;
     a.n_blk = (int)n_blk;
-    a.slab_floats = (int)slab_floats;
     a.stage_floats = (int)stage_floats;
     a.sign = p.sign;
     a.act = p.act;
-    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS, WAVES>),
+    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
 
-// Wide tile (workgroup = WCO x WPOS waves, each MW x NW MFMA tiles).
-// Chosen by measurement on MI355X: k = 2 takes all 64 channels of the 2D
-// workloads in one workgroup (4 x 1 waves of 4 x 8 tiles, 2 waves/SIMD); k = 3
-// does best with smaller 4 x 4 tiles at 3 waves/SIMD.
+// Tile shapes: workgroup = WCO x WPOS waves, each wave MW x NW MFMA tiles
+// (16 x 16 each): WCO * MW * (16 / N_B) output channels by WPOS * NW * 16
+// positions.
+//  wide    the large workloads; chosen by measurement on MI355X: k = 2 takes
+//          all 64 channels in one workgroup (4 x 1 waves of 4 x 8 tiles,
+//          2 waves/SIMD), k = 3 does best with 4 x 4 tiles at 3 waves/SIMD
+//  medium  many channels, few positions: 32 positions per workgroup
+//  narrow  few channels, many positions
+//  tiny    one wave, 4 (k = 2) or 2 (k = 3) channels by 32 positions: small
+//          problems, spread over as many CUs as possible
 #ifndef CLIFF_W2
 #define CLIFF_W2 4, 1, 4, 8, 6, 2  // WCO, WPOS, MW, NW, SLOTS, waves/SIMD (k = 2)
 #endif
 #ifndef CLIFF_W3
 #define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
 #endif
+#define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
+#define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
+#define CLIFF_NARROW 1, 4, 2, 4, 8, 2
+#define CLIFF_TINY2 1, 1, 1, 2, 12, 4
+#define CLIFF_TINY3 1, 1, 1, 2, 12, 3
 
-template <int KD, int NB, int DF, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
-cliff_status run_wide_or_narrow(const ConvProblem& p, hipStream_t stream)
-{
-    // wide: all (or half) of the output channels per workgroup;
-    // narrow: few channels, 256 positions (small C_out).
-    constexpr int CO_WIDE = WCO * MW * (16 / NB);
-    if (p.C_out * 2 > CO_WIDE) {
-        const cliff_status s = run<KD, NB, DF, WCO, WPOS, MW, NW, SLOTS, WAVES>(p, stream);
-        if (s != CLIFF_EUNSUPPORTED) return s;
+template <int NB, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
+struct Shape {
+    static constexpr int co_wg = WCO * MW * (16 / NB);
+    static constexpr int pos = WPOS * NW * 16;
+    static int64_t blocks(const ConvProblem& p, int64_t M)
+    {
+        return (M + pos - 1) / pos * ((p.C_out + co_wg - 1) / co_wg);
     }
-    return run<KD, NB, DF, 1, 4, 2, 4, 8, 2>(p, stream);
+};
+
+template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
+cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream, Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES>)
+{
+    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>(p, stream);
 }
 
 template <int KD, int NB, int DF>
 cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
 {
-    if (KD == 2) return run_wide_or_narrow<KD, NB, DF, CLIFF_W2>(p, stream);
-    return run_wide_or_narrow<KD, NB, DF, CLIFF_W3>(p, stream);
+    using Wide = std::conditional_t<KD == 2, Shape<NB, CLIFF_W2>, Shape<NB, CLIFF_W3>>;
+    using Medium = std::conditional_t<KD == 2, Shape<NB, CLIFF_MEDIUM2>, Shape<NB, CLIFF_MEDIUM3>>;
+    using Narrow = Shape<NB, CLIFF_NARROW>;
+    using Tiny = std::conditional_t<KD == 2, Shape<NB, CLIFF_TINY2>, Shape<NB, CLIFF_TINY3>>;
+    int64_t M = p.B;
+    for (int t = 0; t < KD; ++t) M *= p.d_out;
+    // Shape choice, from timing every shape on 2D/3D convolutions and linear
+    // layers (d_image = d_filter = 1) of 7 to 9,000 GFLOP on MI355X (256 CUs):
+    // wide once it fills every CU; medium for linear layers with >= 128
+    // workgroups; narrow from 128 workgroups; tiny (one wave per workgroup,
+    // the most workgroups) for the smallest problems.  A shape whose LDS or
+    // staging needs do not fit returns CLIFF_EUNSUPPORTED and the next one in
+    // the order is tried.
+    const bool wide_ok = p.C_out * 2 > Wide::co_wg;
+    const bool medium_ok = p.C_out * 2 > Medium::co_wg;
+    const int64_t bw = wide_ok ? Wide::blocks(p, M) : 0;
+    const int64_t bm = medium_ok ? Medium::blocks(p, M) : 0;
+    const int64_t bn = Narrow::blocks(p, M);
+    int first;
+    if (bw >= 256)
+        first = 0;
+    else if (bm >= 128 && p.d_filter == 1)
+        first = 1;
+    else if (bn >= 128)
+        first = 2;
+    else if (bm >= 128)
+        first = 1;
+    else
+        first = 3;
+    int order[4] = {first, 0, 2, 1};
+    int n_order = 4;
+    if (p.mfma_shape >= 0) {
+        order[0] = p.mfma_shape;  // forced by the caller
+        n_order = 1;
+    }
+    // the 3x3(x3) wide kernels stage one input channel at a time (a stage
+    // already holds 288 MFMAs per wave, and the fixed count keeps their
+    // register use down); the other shapes choose the channels per stage at
+    // run time
+    constexpr int WCC = DF == 3 ? 1 : 0;
+    for (int i = 0; i < n_order; ++i) {
+        const int o = order[i];
+        if (i > 0 && o == order[0]) continue;
+        const bool forced = p.mfma_shape >= 0;
+        cliff_status s = CLIFF_EUNSUPPORTED;
+        if (o == 0 && (wide_ok || forced)) s = run_shape_cfg<KD, NB, DF, WCC>(p, stream, Wide{});
+        if (o == 1 && (medium_ok || forced)) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Medium{});
+        if (o == 2) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Narrow{});
+        if (o == 3) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Tiny{});
+        if (s != CLIFF_EUNSUPPORTED) return s;
+    }
+    if (p.mfma_shape < 0 && first != 3)
+        return run_shape_cfg<KD, NB, DF, 0>(p, stream, Tiny{});
+    return CLIFF_EUNSUPPORTED;
 }
 
 }  // namespace

@@ -33,6 +33,9 @@ SHAPES2 = [
     (3, 5, 70, 20, 3),    # two channel blocks, ragged positions
     (1, 2, 9, 7, 1),      # pointwise (linear-layer-like)
     (2, 3, 5, 6, 6),      # d_out = 1
+    (5, 13, 9, 3, 3),     # several channels per stage, partial last group
+    (64, 37, 64, 1, 1),   # linear layer (Algorithm 2 as d_image = d_filter = 1)
+    (300, 64, 64, 1, 1),  # linear layer, several position blocks
 ]
 SHAPES3 = [
     (1, 1, 1, 4, 3),
@@ -40,6 +43,8 @@ SHAPES3 = [
     (3, 2, 5, 7, 2),
     (1, 4, 3, 9, 5),
     (2, 2, 4, 3, 1),
+    (8, 4, 4, 16, 3),     # several channels per stage
+    (64, 37, 64, 1, 1),   # linear layer
 ]
 
 
@@ -48,8 +53,12 @@ def _case(seed, g, shape):
     return random_conv_case(seed, len(g), g, B, C_in, C_out, d_image, d_filter)
 
 
-@pytest.mark.parametrize("algo", [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT],
-                         ids=["auto", "mfma", "direct"])
+ALGOS = [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM,
+         P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY]
+ALGO_IDS = ["auto", "mfma", "direct", "wide", "medium", "narrow", "tiny"]
+
+
+@pytest.mark.parametrize("algo", ALGOS, ids=ALGO_IDS)
 @pytest.mark.parametrize("shape", SHAPES2, ids=str)
 def test_conv2d_parity(algo, shape):
     g = (1, 1)
@@ -61,8 +70,8 @@ def test_conv2d_parity(algo, shape):
 
 
 def _run_allow_unsupported(g, x, f, b, algo, act=None):
-    """MFMA forced may legitimately refuse shapes whose slab does not fit."""
-    if algo != P.ALGO_MFMA:
+    """A forced MFMA tiling may legitimately refuse shapes it cannot stage."""
+    if algo < P.ALGO_MFMA:
         return gpu_conv(g, x, f, b, act=act, algo=algo)
     try:
         return gpu_conv(g, x, f, b, act=act, algo=algo)
@@ -72,8 +81,7 @@ def _run_allow_unsupported(g, x, f, b, algo, act=None):
         raise
 
 
-@pytest.mark.parametrize("algo", [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT],
-                         ids=["auto", "mfma", "direct"])
+@pytest.mark.parametrize("algo", ALGOS, ids=ALGO_IDS)
 @pytest.mark.parametrize("shape", SHAPES3, ids=str)
 def test_conv3d_parity(algo, shape):
     g = (1, 1, 1)
@@ -89,7 +97,7 @@ def test_all_signatures(g):
     shape = (2, 3, 6, 9, 3) if len(g) == 2 else (2, 3, 3, 6, 3)
     s, x, f, b = _case(102, g, shape)
     ref = oracle.conv_nd(x, f, b, g)
-    for algo in (P.ALGO_MFMA, P.ALGO_DIRECT):
+    for algo in (P.ALGO_MFMA, P.ALGO_DIRECT, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_TINY):
         assert_parity(gpu_conv(g, x, f, b, algo=algo), ref, what="%s algo %d" % (g, algo))
 
 
@@ -130,13 +138,20 @@ def _act_args(seed, C, mode, blades):
     return aw, ab
 
 
-@pytest.mark.parametrize("algo", [P.ALGO_MFMA, P.ALGO_DIRECT], ids=["mfma", "direct"])
+FUSED_ALGOS = [P.ALGO_MFMA, P.ALGO_DIRECT, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM,
+               P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY]
+FUSED_IDS = ["mfma", "direct", "wide", "medium", "narrow", "tiny"]
+
+
+@pytest.mark.parametrize("algo", FUSED_ALGOS, ids=FUSED_IDS)
 @pytest.mark.parametrize("mode,blades", ACTS, ids=str)
 def test_fused_act_2d(algo, mode, blades):
     g = (1, -1)
     s, x, f, b = _case(106, g, (3, 5, 70, 12, 3))
     aw, ab = _act_args(5, 70, mode, blades)
-    y = gpu_conv(g, x, f, b, act=(mode, blades, aw, ab), algo=algo)
+    y = _run_allow_unsupported(g, x, f, b, algo, act=(mode, blades, aw, ab))
+    if y is None:
+        return
     ref = oracle.act(oracle.conv_nd(x, f, b, g), mode, blades, aw, ab)
     assert_parity(y, ref)
 
@@ -145,13 +160,15 @@ ACTS3 = [(AGG_MEAN, tuple(range(8))), (AGG_LINEAR, tuple(range(8))),
          (AGG_SUM, (7, 0, 4)), (AGG_LINEAR, (3, 5)), (AGG_MEAN, (6,))]
 
 
-@pytest.mark.parametrize("algo", [P.ALGO_MFMA, P.ALGO_DIRECT], ids=["mfma", "direct"])
+@pytest.mark.parametrize("algo", FUSED_ALGOS, ids=FUSED_IDS)
 @pytest.mark.parametrize("mode,blades", ACTS3, ids=str)
 def test_fused_act_3d(algo, mode, blades):
     g = (1, 1, 1)
     s, x, f, b = _case(107, g, (2, 3, 33, 8, 3))
     aw, ab = _act_args(6, 33, mode, blades)
-    y = gpu_conv(g, x, f, b, act=(mode, blades, aw, ab), algo=algo)
+    y = _run_allow_unsupported(g, x, f, b, algo, act=(mode, blades, aw, ab))
+    if y is None:
+        return
     ref = oracle.act(oracle.conv_nd(x, f, b, g), mode, blades, aw, ab)
     assert_parity(y, ref)
 
