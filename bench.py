@@ -160,6 +160,47 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
     return res
 
 
+def measure_act(nb: int, B: int, C: int, Pn: int, mode: int, blades, steps: int = 20,
+                warmup: int = 3, inplace: bool = False):
+    """Standalone multivector activation on [B, C, P, N_B]: mean kernel time
+    (HIP events on the launch stream) and HBM rate of its algorithmic bytes
+    (input read once, output written once)."""
+    import torch
+    import paper_2507_01040_amd as P
+    g = torch.Generator(device="cuda:0").manual_seed(1234)
+    x = torch.randn((B, C, Pn, nb), device="cuda:0", generator=g)
+    aw = torch.randn((C, len(blades)), device="cuda:0", generator=g)
+    ab = 0.1 * torch.randn((C,), device="cuda:0", generator=g)
+    y = x if inplace else torch.empty_like(x)
+    desc = P.make_act_desc(mode, blades, aw.data_ptr(), ab.data_ptr())
+    stream = torch.cuda.current_stream().cuda_stream
+    call = lambda: P.multivector_act(nb, B, C, Pn, desc, x.data_ptr(), y.data_ptr(), stream)
+    for _ in range(warmup):
+        assert call() == P.CLIFF_OK
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record()
+        call()
+        e1.record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    # a plain device copy of the same bytes: the HBM rate reachable in practice
+    z = torch.empty_like(x)
+    for e0, e1 in ev:
+        e0.record()
+        z.copy_(x)
+        e1.record()
+    torch.cuda.synchronize()
+    ms_copy = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    nbytes = 2 * x.numel() * 4
+    return {"shape": [B, C, Pn, nb], "mode": W.AGG_NAMES[mode], "K": len(blades),
+            "inplace": inplace, "kernel_ms": round(ms, 4), "bytes": nbytes,
+            "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "device_copy_GB_s": round(nbytes / (ms_copy * 1e-3) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -234,6 +275,12 @@ def main():
                                   epilogue_overhead=True)
             torch.cuda.empty_cache()
         line["workloads"] = extra
+        # standalone activation at the blocks' intermediate shapes (HBM bound)
+        line["multivector_act"] = [
+            measure_act(4, 8, 64, 128 * 128, W.AGG_LINEAR, (0, 1, 2, 3)),
+            measure_act(8, 8, 64, 34 ** 3, W.AGG_MEAN, tuple(range(8))),
+            measure_act(8, 8, 64, 34 ** 3, W.AGG_MEAN, tuple(range(8)), inplace=True),
+        ]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)

@@ -1,53 +1,107 @@
-// Standalone multivector activation (paper, Algorithm 3) on [B, C, P, N_B]:
-// one thread per multivector, the gate computed once per multivector (not
-// once per blade), blades loaded and stored as 16-byte vectors.  The kernel
-// streams its input once and its output once, so HBM bandwidth bounds it.
+// Standalone multivector activation (paper, Algorithm 3) on [B, C, P, N_B].
+//
+// The kernel streams its input once and its output once, so HBM bandwidth
+// bounds it (8 N_B bytes per multivector).  Each workgroup owns a run of
+// positions of one (b, c) pair, so the channel's gate weights and bias are
+// uniform (scalar loads, computed once per workgroup), and each thread issues
+// all loads of its VPT multivectors before any arithmetic.  The gate is
+// computed once per multivector, not once per blade.  Data that is read or
+// written once is accessed non-temporally.
 #include "common.hpp"
 #include "epilogue.hpp"
 
 namespace cliff {
 namespace {
 
+typedef float vf2 __attribute__((ext_vector_type(2)));
+typedef float vf4 __attribute__((ext_vector_type(4)));
+
+#ifndef CLIFF_ACT_VPT
+#define CLIFF_ACT_VPT 2  // measured: 2 is best or tied at 0.27-1.3 GB per call
+#endif
+constexpr int ACT_THREADS = 256;
+constexpr int ACT_VPT = CLIFF_ACT_VPT;  // multivectors per thread
+
 struct ActKArgs {
     const float* x;
     float* y;
-    int64_t n;  // B * C * P multivectors
-    int64_t C, P;
+    int64_t P;       // positions per (b, c)
+    int64_t n_pblk;  // workgroups per (b, c)
+    int C;
     ActParams act;
 };
 
 template <int NB>
-__global__ __launch_bounds__(256) void act_kernel(ActKArgs a)
-{
-    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (t >= a.n) return;
-    const int c = (int)((t / a.P) % a.C);
+struct MV {
     float v[NB];
-    if (NB == 2) {
-        const float2 u = reinterpret_cast<const float2*>(a.x)[t];
-        v[0] = u.x;
-        v[1] = u.y;
+};
+
+template <int NB>
+__device__ inline MV<NB> load_mv(const float* p)
+{
+    MV<NB> m;
+    if constexpr (NB == 2) {
+        const vf2 u = __builtin_nontemporal_load(reinterpret_cast<const vf2*>(p));
+        m.v[0] = u.x;
+        m.v[1] = u.y;
     } else {
 #pragma unroll
         for (int h = 0; h < NB / 4; ++h) {
-            const float4 u = reinterpret_cast<const float4*>(a.x)[t * (NB / 4) + h];
-            v[4 * h + 0] = u.x;
-            v[4 * h + 1] = u.y;
-            v[4 * h + 2] = u.z;
-            v[4 * h + 3] = u.w;
+            const vf4 u = __builtin_nontemporal_load(reinterpret_cast<const vf4*>(p) + h);
+            m.v[4 * h + 0] = u.x;
+            m.v[4 * h + 1] = u.y;
+            m.v[4 * h + 2] = u.z;
+            m.v[4 * h + 3] = u.w;
         }
     }
-    float part = 0.f;
-#pragma unroll
-    for (int i = 0; i < NB; ++i) part += gate_coef(a.act, gate_slot(a.act, i), c) * v[i];
-    const float g = gate_sigmoid(a.act, part, c);
-    if (NB == 2) {
-        reinterpret_cast<float2*>(a.y)[t] = make_float2(v[0] * g, v[1] * g);
+    return m;
+}
+
+template <int NB>
+__device__ inline void store_mv(float* p, const MV<NB>& m)
+{
+    if constexpr (NB == 2) {
+        __builtin_nontemporal_store(vf2{m.v[0], m.v[1]}, reinterpret_cast<vf2*>(p));
     } else {
 #pragma unroll
         for (int h = 0; h < NB / 4; ++h)
-            reinterpret_cast<float4*>(a.y)[t * (NB / 4) + h] =
-                make_float4(v[4 * h] * g, v[4 * h + 1] * g, v[4 * h + 2] * g, v[4 * h + 3] * g);
+            __builtin_nontemporal_store(
+                vf4{m.v[4 * h], m.v[4 * h + 1], m.v[4 * h + 2], m.v[4 * h + 3]},
+                reinterpret_cast<vf4*>(p) + h);
+    }
+}
+
+template <int NB>
+__global__ __launch_bounds__(ACT_THREADS) void act_kernel(ActKArgs a)
+{
+    const int64_t bc = blockIdx.x / a.n_pblk;  // (b, c) of this workgroup
+    const int64_t pblk = blockIdx.x - bc * a.n_pblk;
+    const int c = (int)(bc % a.C);
+    float coef[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) coef[i] = gate_coef(a.act, gate_slot(a.act, i), c);
+
+    const int64_t p0 = pblk * (ACT_THREADS * ACT_VPT) + threadIdx.x;
+    const float* xb = a.x + bc * a.P * NB;
+    float* yb = a.y + bc * a.P * NB;
+    MV<NB> m[ACT_VPT];
+#pragma unroll
+    for (int v = 0; v < ACT_VPT; ++v) {
+        const int64_t p = p0 + v * ACT_THREADS;
+        if (p < a.P) m[v] = load_mv<NB>(xb + p * NB);
+    }
+#pragma unroll
+    for (int v = 0; v < ACT_VPT; ++v) {
+        const int64_t p = p0 + v * ACT_THREADS;
+        if (p < a.P) {
+            float part = 0.f;
+#pragma unroll
+            for (int i = 0; i < NB; ++i) part += coef[i] * m[v].v[i];
+            const float g = gate_sigmoid(a.act, part, c);
+#pragma unroll
+            for (int i = 0; i < NB; ++i) m[v].v[i] *= g;
+            store_mv<NB>(yb + p * NB, m[v]);
+        }
     }
 }
 
@@ -59,16 +113,16 @@ cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P, const ActParams
     ActKArgs a;
     a.x = x;
     a.y = y;
-    a.n = B * C * P;
-    a.C = C;
     a.P = P;
+    a.n_pblk = (P + ACT_THREADS * ACT_VPT - 1) / (ACT_THREADS * ACT_VPT);
+    a.C = (int)C;
     a.act = act;
-    const int64_t blocks = (a.n + 255) / 256;
-    if (blocks >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
+    const int64_t blocks = a.n_pblk * B * C;
+    if (blocks >= (1ll << 31) || C >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
     switch (nb) {
-    case 2: hipLaunchKernelGGL(act_kernel<2>, dim3((unsigned)blocks), dim3(256), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL(act_kernel<4>, dim3((unsigned)blocks), dim3(256), 0, stream, a); break;
-    case 8: hipLaunchKernelGGL(act_kernel<8>, dim3((unsigned)blocks), dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(act_kernel<2>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL(act_kernel<4>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;
+    case 8: hipLaunchKernelGGL(act_kernel<8>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;
     default: return CLIFF_EUNSUPPORTED;
     }
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
