@@ -201,6 +201,36 @@ def measure_act(nb: int, B: int, C: int, Pn: int, mode: int, blades, steps: int 
             "device_copy_GB_s": round(nbytes / (ms_copy * 1e-3) / 1e9, 1)}
 
 
+def measure_linear(k: int, B: int, C: int, steps: int = 20, warmup: int = 3):
+    """Clifford linear layer (Algorithm 2) [B, C, N_B] x [C, C, N_B]: mean
+    kernel time and useful TFLOP/s (2 B C^2 N_B^2 FLOPs)."""
+    import torch
+    import paper_2507_01040_amd as P
+    nb = 1 << k
+    g = (1,) * k
+    gen = torch.Generator(device="cuda:0").manual_seed(99)
+    x = torch.randn((B, C, nb), device="cuda:0", generator=gen)
+    w = torch.rand((C, C, nb), device="cuda:0", generator=gen) / C
+    b = torch.randn((C, nb), device="cuda:0", generator=gen)
+    out = torch.empty((B, C, nb), device="cuda:0")
+    for _ in range(warmup):
+        P.linear(x, w, b, g, out=out)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for e0, e1 in ev:
+        e0.record()
+        P.linear(x, w, b, g, out=out)
+        e1.record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    flops = 2 * B * C * C * nb * nb
+    nbytes = 4 * (x.numel() + w.numel() + b.numel() + out.numel())
+    return {"k": k, "B": B, "C_in": C, "C_out": C, "kernel_ms": round(ms, 4),
+            "useful_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+            "frac_of_fp32_mfma_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4),
+            "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -275,6 +305,8 @@ def main():
                                   epilogue_overhead=True)
             torch.cuda.empty_cache()
         line["workloads"] = extra
+        # Clifford linear layers at the paper's C = 32 with GPU-sized batches
+        line["clifford_linear"] = [measure_linear(2, 1 << 20, 32), measure_linear(3, 1 << 19, 32)]
         # standalone activation at the blocks' intermediate shapes (HBM bound)
         line["multivector_act"] = [
             measure_act(4, 8, 64, 128 * 128, W.AGG_LINEAR, (0, 1, 2, 3)),

@@ -118,8 +118,9 @@ typedef enum {
     CLIFF_ALGO_DIRECT = 1,      /* one thread per output multivector, fp32 FMA */
     CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA (k = 2, 3 only),
                                    tile shape chosen from the problem size */
-    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=2) / 16 (k=3)
-                                   channels x 128 positions per workgroup */
+    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=2; 32 x 256 when
+                                   C_out <= 32) / 16 (k=3) channels x 128
+                                   positions per workgroup */
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 32 channels x 32 positions */
     CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 4 channels x 256 positions */
     CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 4 / 2 channels x 32 positions, one wave */
@@ -137,6 +138,26 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
                                    const float* filters, const float* bias,
                                    float* output, const cliff_act_desc* act,
                                    void* stream, int algo);
+
+/*
+ * Clifford linear layer (paper, Algorithm 2), plus the bias add and, if
+ * `act` is not NULL, the fused multivector activation:
+ *
+ *   output[b, co] = act( sum_{ci} weight[ci, co] * input[b, ci] + bias[co] )
+ *
+ * with the weight on the left of the geometric product.
+ *   k, g      as for clifford_conv_nd (k = 1 runs on the per-output kernel)
+ *   input     device [B, C_in, N_B]
+ *   weight    device [C_in, C_out, N_B]
+ *   bias      device [C_out, N_B], or NULL for zero
+ *   output    device [B, C_out, N_B]; must not overlap any input
+ * Same alignment, size, error and stream rules as clifford_conv_nd; it is
+ * the convolution with d_image = d_filter = 1 and runs on the same kernels.
+ */
+cliff_status clifford_linear(int k, const int8_t* g, int64_t B, int64_t C_in,
+                             int64_t C_out, const float* input, const float* weight,
+                             const float* bias, float* output,
+                             const cliff_act_desc* act, void* stream);
 
 /*
  * Standalone multivector activation (paper, Algorithm 3).

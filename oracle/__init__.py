@@ -5,7 +5,7 @@ benchmark's ``cpu_baseline`` leg use it; the GPU library never does.  It
 shares no code with the GPU path.
 
 The arithmetic lives in ``cliff_oracle.c`` (plain C, fp64, following the
-definitions of the paper's "Background" section and Algorithms 1 and 3).  This
+definitions of the paper's "Background" section and Algorithms 1, 2 and 3).  This
 module compiles it with gcc into ``liboracle.so`` next to it and marshals numpy
 arrays in and out; it adds no arithmetic of its own (inputs are only widened
 to float64 and cropped by slicing).
@@ -53,8 +53,9 @@ def _load():
                                            i64, p, p, p, i64, p, p, p, p]
         lib.oracle_act.argtypes = [ctypes.c_int, i64, i64, i64, ctypes.c_int,
                                    ctypes.c_int, p, p, p, p, p]
+        lib.oracle_linear.argtypes = [ctypes.c_int, p, i64, i64, i64, p, p, p, p]
         for f in (lib.oracle_cayley, lib.oracle_mv_mul, lib.oracle_conv_nd,
-                  lib.oracle_conv_points, lib.oracle_act):
+                  lib.oracle_conv_points, lib.oracle_act, lib.oracle_linear):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -149,6 +150,23 @@ def conv_points(x, f, bias, g: Sequence[int], bs, cos, ps) -> np.ndarray:
                                     _ptr(bs), _ptr(cos), _ptr(ps), _ptr(out))
     if rc:
         raise ValueError("oracle_conv_points rejected the arguments")
+    return out
+
+
+def linear(x, w, bias, g: Sequence[int]) -> np.ndarray:
+    """Algorithm 2 in fp64: x [B, C_in, N_B], w [C_in, C_out, N_B], bias
+    [C_out, N_B] or None.  Returns [B, C_out, N_B] float64."""
+    k = len(g)
+    x, w = _f64(x), _f64(w)
+    b = None if bias is None else _f64(bias)
+    B, C_in, nb = x.shape
+    C_out = w.shape[1]
+    assert nb == 1 << k and w.shape == (C_in, C_out, nb), (x.shape, w.shape)
+    out = np.empty((B, C_out, nb), np.float64)
+    gg = _g(g)
+    if _load().oracle_linear(k, _ptr(gg), B, C_in, C_out, _ptr(x), _ptr(w), _ptr(b),
+                             _ptr(out)):
+        raise ValueError("oracle_linear rejected the arguments")
     return out
 
 

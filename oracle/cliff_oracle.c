@@ -1,6 +1,7 @@
 /*
- * Plain, slow fp64 reference ("oracle") for the Clifford convolution and the
- * multivector activation of "Fast Clifford Neural Layers" (arXiv 2507.01040).
+ * Plain, slow fp64 reference ("oracle") for the Clifford convolution, the
+ * Clifford linear layer and the multivector activation of "Fast Clifford
+ * Neural Layers" (arXiv 2507.01040).
  *
  * TEST INFRASTRUCTURE ONLY.  This file exists to check the GPU library.  It
  * shares no code, header, table or constant with it, and the GPU library must
@@ -354,5 +355,33 @@ int oracle_act(int nb, int64_t B, int64_t C, int64_t P, int mode, int K,
                 double sig = 1.0 / (1.0 + exp(-s));
                 for (int j = 0; j < nb; ++j) y[j] = x[j] * sig;
             }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 2: Clifford linear layer.                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Public.  input [B, C_in, N_B], weight [C_in, C_out, N_B], bias [C_out, N_B]
+ * or NULL; output [B, C_out, N_B]:
+ *   output[b, co] = sum_ci weight[ci, co] * input[b, ci] + bias[co]
+ * (geometric product, weight on the left). */
+int oracle_linear(int k, const int* g, int64_t B, int64_t C_in, int64_t C_out,
+                  const double* input, const double* weight, const double* bias,
+                  double* output)
+{
+    if (k < 1 || k > MAXK || B < 0 || C_in < 1 || C_out < 1) return -1;
+    cayley t;
+    make_cayley(k, g, &t);
+    const int nb = t.nb;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t co = 0; co < C_out; ++co) {
+            double o[MAXNB];
+            for (int i = 0; i < nb; ++i) o[i] = 0.0;
+            for (int64_t ci = 0; ci < C_in; ++ci)
+                mv_mul_acc(&t, weight + (ci * C_out + co) * nb, input + (b * C_in + ci) * nb, o);
+            for (int i = 0; i < nb; ++i)
+                output[(b * C_out + co) * nb + i] = o[i] + (bias ? bias[co * nb + i] : 0.0);
+        }
     return 0;
 }

@@ -26,8 +26,8 @@ AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
 ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
 ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
 
-EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "multivector_act",
-            "cliffconv_cayley_table", "cliffconv_status_string")
+EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
+            "multivector_act", "cliffconv_cayley_table", "cliffconv_status_string")
 
 
 class CliffActDesc(ctypes.Structure):
@@ -60,13 +60,15 @@ def load(path: str = LIB_PATH):
                  ctypes.POINTER(CliffActDesc), vp]
     lib.clifford_conv_nd.argtypes = conv_args
     lib.clifford_conv_nd_algo.argtypes = conv_args + [i32]
+    lib.clifford_linear.argtypes = [i32, vp, i64, i64, i64, vp, vp, vp, vp,
+                                    ctypes.POINTER(CliffActDesc), vp]
     lib.multivector_act.argtypes = [i32, i64, i64, i64,
                                     ctypes.POINTER(CliffActDesc), vp, vp, vp]
     lib.cliffconv_cayley_table.argtypes = [i32, vp, vp, vp]
     lib.cliffconv_status_string.argtypes = [i32]
     lib.cliffconv_status_string.restype = ctypes.c_char_p
-    for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "multivector_act",
-                 "cliffconv_cayley_table"):
+    for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
+                 "multivector_act", "cliffconv_cayley_table"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -117,6 +119,15 @@ def clifford_conv_nd_algo(k: int, g: Sequence[int], B: int, C_in: int,
         k, _g_array(g), B, C_in, C_out, d_image, d_filter, input_ptr or None,
         filters_ptr or None, bias_ptr or None, output_ptr or None,
         ctypes.byref(act) if act is not None else None, stream or None, algo)
+
+
+def clifford_linear(k: int, g: Sequence[int], B: int, C_in: int, C_out: int,
+                    input_ptr: int, weight_ptr: int, bias_ptr: int, output_ptr: int,
+                    act: Optional[CliffActDesc] = None, stream: int = 0) -> int:
+    return load().clifford_linear(
+        k, _g_array(g), B, C_in, C_out, input_ptr or None, weight_ptr or None,
+        bias_ptr or None, output_ptr or None,
+        ctypes.byref(act) if act is not None else None, stream or None)
 
 
 def multivector_act(nb: int, B: int, C: int, P: int, act: CliffActDesc,
@@ -186,6 +197,32 @@ def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
                                out.data_ptr(), desc, _stream_ptr(stream), algo)
     if st != CLIFF_OK:
         raise CliffError(st, "clifford_conv_nd")
+    return out
+
+
+def linear(x, weight, bias, g: Sequence[int], act: Optional[Tuple] = None,
+           out=None, stream=None):
+    """Clifford linear layer of GPU tensors x [B, C_in, N_B], weight
+    [C_in, C_out, N_B], bias [C_out, N_B] or None; ``act`` as for conv_nd."""
+    import torch
+    k = len(g)
+    _check_dev(x, "x")
+    _check_dev(weight, "weight")
+    if bias is not None:
+        _check_dev(bias, "bias")
+    B, C_in, C_out = x.shape[0], x.shape[1], weight.shape[1]
+    if out is None:
+        out = torch.empty((B, C_out, 1 << k), dtype=torch.float32, device=x.device)
+    desc = None
+    if act is not None:
+        mode, blades, aw, ab = act
+        desc = make_act_desc(mode, blades, aw.data_ptr() if aw is not None else 0,
+                             ab.data_ptr() if ab is not None else 0)
+    st = clifford_linear(k, g, B, C_in, C_out, x.data_ptr(), weight.data_ptr(),
+                         bias.data_ptr() if bias is not None else 0, out.data_ptr(),
+                         desc, _stream_ptr(stream))
+    if st != CLIFF_OK:
+        raise CliffError(st, "clifford_linear")
     return out
 
 

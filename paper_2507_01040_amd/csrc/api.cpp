@@ -206,6 +206,15 @@ cliff_status clifford_conv_nd(int k, const int8_t* g, int64_t B, int64_t C_in, i
                                  output, act, stream, CLIFF_ALGO_AUTO);
 }
 
+cliff_status clifford_linear(int k, const int8_t* g, int64_t B, int64_t C_in, int64_t C_out,
+                             const float* input, const float* weight, const float* bias,
+                             float* output, const cliff_act_desc* act, void* stream)
+{
+    // Algorithm 2 is Algorithm 1 with a single position and a single tap
+    return clifford_conv_nd_algo(k, g, B, C_in, C_out, 1, 1, input, weight, bias, output, act,
+                                 stream, CLIFF_ALGO_AUTO);
+}
+
 cliff_status multivector_act(int nb, int64_t B, int64_t C, int64_t P,
                              const cliff_act_desc* act, const float* input, float* output,
                              void* stream)

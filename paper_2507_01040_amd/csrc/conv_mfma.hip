@@ -427,6 +427,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #ifndef CLIFF_W3
 #define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
 #endif
+#define CLIFF_W2_32 2, 2, 4, 8, 6, 2  // k = 2 wide variant for C_out <= 32
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
 #define CLIFF_NARROW 1, 4, 2, 4, 8, 2
@@ -449,10 +450,25 @@ cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream, Shape<NB, W
     return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>(p, stream);
 }
 
+template <int KD, int NB, int DF, class Wide>
+cliff_status run_shapes(const ConvProblem& p, hipStream_t stream);
+
 template <int KD, int NB, int DF>
 cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
 {
-    using Wide = std::conditional_t<KD == 2, Shape<NB, CLIFF_W2>, Shape<NB, CLIFF_W3>>;
+    // k = 2 has two wide tiles: 64 channels x 128 positions, and for
+    // C_out <= 32 a 32 x 256 one, so the channels are not half wasted
+    if constexpr (KD == 2) {
+        if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32>>(p, stream);
+        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2>>(p, stream);
+    } else {
+        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3>>(p, stream);
+    }
+}
+
+template <int KD, int NB, int DF, class Wide>
+cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
+{
     using Medium = std::conditional_t<KD == 2, Shape<NB, CLIFF_MEDIUM2>, Shape<NB, CLIFF_MEDIUM3>>;
     using Narrow = Shape<NB, CLIFF_NARROW>;
     using Tiny = std::conditional_t<KD == 2, Shape<NB, CLIFF_TINY2>, Shape<NB, CLIFF_TINY3>>;

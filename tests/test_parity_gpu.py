@@ -232,3 +232,26 @@ def test_errors_with_real_buffers():
                               xt.data_ptr()) == P.CLIFF_EOVERLAP
     # untouched output after an error
     assert float(out.abs().sum()) == 0.0
+
+
+@pytest.mark.parametrize("g,B,C_in,C_out", [((-1,), 37, 5, 3), ((1, 1), 300, 32, 32),
+                                          ((1, -1), 4096, 64, 64), ((1, 1, 1), 513, 17, 40),
+                                          ((0, -1, 1), 64, 8, 8)], ids=str)
+def test_linear_parity(g, B, C_in, C_out):
+    import torch
+    k = len(g)
+    nb = 1 << k
+    rng = np.random.default_rng(300 + B)
+    x = rng.standard_normal((B, C_in, nb)).astype(np.float32)
+    w = rng.uniform(-1 / np.sqrt(C_in), 1 / np.sqrt(C_in), (C_in, C_out, nb)).astype(np.float32)
+    b = rng.standard_normal((C_out, nb)).astype(np.float32)
+    ref = oracle.linear(x, w, b, g)
+    y = P.linear(dev(x), dev(w), dev(b), g)
+    torch.cuda.synchronize()
+    assert_parity(y.cpu().numpy(), ref)
+    # fused activation
+    aw, ab = _act_args(8, C_out, AGG_LINEAR, tuple(range(nb)))
+    y = P.linear(dev(x), dev(w), dev(b), g, act=(AGG_LINEAR, tuple(range(nb)), dev(aw), dev(ab)))
+    torch.cuda.synchronize()
+    assert_parity(y.cpu().numpy(), oracle.act(ref[:, :, None, :], AGG_LINEAR, tuple(range(nb)),
+                                              aw, ab)[:, :, 0, :])
