@@ -200,3 +200,10 @@ def random_act_case(seed: int, nb: int, B: int, C: int, P: int, mode: int,
     aw = _normal(rng, (C, K)) if mode == AGG_LINEAR else None
     ab = _normal(rng, (C,), 0.1) if mode == AGG_LINEAR else None
     return x, ActSpec(mode, blades), aw, ab
+
+
+def batch_entry_normal(seed: int, b: int, entry_shape) -> np.ndarray:
+    """N(0,1) float32 values of batch entry b of a large input, drawn from
+    its own stream (seed, b), so any entry can be regenerated alone."""
+    rng = np.random.default_rng([seed, b])
+    return rng.standard_normal(size=tuple(entry_shape), dtype=np.float32)
