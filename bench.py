@@ -94,6 +94,28 @@ class Runner:
                 events[li][1].record()
         return y
 
+    def time_graph(self, steps: int, warmup: int):
+        """The step captured once in a HIP graph and replayed: per-step time
+        without the host launch path (matters only for tiny workloads)."""
+        torch = self.torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(max(1, warmup)):
+                self.step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.step()
+        for _ in range(warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps * 1e3
+
     def time(self, steps: int, warmup: int):
         torch = self.torch
         for _ in range(warmup):
@@ -150,6 +172,7 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
            "kernel_tflops": [round(l.useful_flops() / (t * 1e-3) / 1e12, 2)
                              for l, t in zip(w.layers, per_layer)]}
     res["frac_of_fp32_mfma_peak"] = round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
+    res["graph_ms_per_step"] = round(r.time_graph(max(steps, 20), warmup), 4)
     if epilogue_overhead and any(a is not None for a in w.acts):
         plain = Runner(w, fuse_act=False)
         ms_plain, per_plain = plain.time(steps, warmup)

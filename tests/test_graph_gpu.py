@@ -1,0 +1,43 @@
+"""The library's launches captured in a HIP graph (through torch.cuda.graph):
+replays must equal the eager results bit for bit (the kernels are
+deterministic), with eager work and synchronisations between replays and
+the inputs changed between replays.  The library records no memset or
+allocation, only kernel launches on the caller's stream."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2507_01040_amd as P
+import workloads as W
+from gpu_util import dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_graph_replay_matches_eager(k):
+    g = (1, -1) if k == 2 else (1, 1, 1)
+    nb = 1 << k
+    s, x, f, b = W.random_conv_case(500 + k, k, g, 3, 8, 40, 14 if k == 2 else 9, 3)
+    rng = np.random.default_rng(7)
+    aw = rng.standard_normal((40, nb)).astype(np.float32)
+    ab = rng.standard_normal(40).astype(np.float32)
+    xt, ft, bt, awt, abt = dev(x), dev(f), dev(b), dev(aw), dev(ab)
+    act = (P.AGG_LINEAR, tuple(range(nb)), awt, abt)
+    out_g = torch.empty(s.output_shape(), device="cuda:0")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm up on the capture stream
+        P.conv_nd(xt, ft, bt, g, act=act, out=out_g)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.conv_nd(xt, ft, bt, g, act=act, out=out_g)
+    for rep in range(3):
+        # new input values, eager reference, then a replay
+        xt.copy_(dev(x * (1.0 + 0.25 * rep)))
+        eager = P.conv_nd(xt, ft, bt, g, act=act)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, eager), "replay %d differs from eager" % rep
