@@ -31,6 +31,8 @@
  *    CLIFF_EDEVICE reports a HIP launch error (hipGetLastError) after the
  *    launch; the output content is then undefined.
  *  - Thread safety: calls may be made concurrently from several host threads.
+ *  - With the environment variable CLIFFCONV_DEBUG set (non-zero), every
+ *    kernel launch prints its kernel, grid and tiling to stderr.
  */
 #ifndef CLIFFCONV_H
 #define CLIFFCONV_H

@@ -7,6 +7,8 @@
 // all loads of its VPT multivectors before any arithmetic.  The gate is
 // computed once per multivector, not once per blade.  Data that is read or
 // written once is accessed non-temporally.
+#include <stdio.h>
+
 #include "common.hpp"
 #include "epilogue.hpp"
 
@@ -119,6 +121,9 @@ cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P, const ActParams
     a.act = act;
     const int64_t blocks = a.n_pblk * B * C;
     if (blocks >= (1ll << 31) || C >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
+    if (debug_enabled())
+        fprintf(stderr, "cliffconv: multivector_act N_B=%d, %lld workgroups of %d\n", nb,
+                (long long)blocks, ACT_THREADS);
     switch (nb) {
     case 2: hipLaunchKernelGGL(act_kernel<2>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;
     case 4: hipLaunchKernelGGL(act_kernel<4>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;

@@ -2,11 +2,25 @@
 // kernel dispatch.  No device memory is allocated here; every call only
 // enqueues kernels on the caller's stream.
 #include <stdint.h>
+#include <stdlib.h>
 
 #include <initializer_list>
 
 #include "cliffconv.h"
 #include "common.hpp"
+
+namespace cliff {
+
+bool debug_enabled()
+{
+    static const bool on = [] {
+        const char* v = getenv("CLIFFCONV_DEBUG");
+        return v && v[0] && !(v[0] == '0' && v[1] == 0);
+    }();
+    return on;
+}
+
+}  // namespace cliff
 
 namespace {
 

@@ -57,6 +57,10 @@ struct ConvProblem {
     int mfma_shape;  // -1: chosen from the problem; 0..3: wide, medium, narrow, tiny
 };
 
+// Launch logging: with the environment variable CLIFFCONV_DEBUG set to a
+// non-zero value, every launch prints its kernel, grid and tiling to stderr.
+bool debug_enabled();
+
 // host-side launchers (defined in the .hip files)
 cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
 // Returns CLIFF_EUNSUPPORTED without launching when no MFMA tiling fits.

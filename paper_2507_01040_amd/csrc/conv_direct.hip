@@ -4,6 +4,8 @@
 // and the fallback for shapes whose slab does not fit the matrix-core tiling.
 // Consecutive threads own consecutive positions of one (b, co), so the
 // multivector loads of a wavefront are contiguous.
+#include <stdio.h>
+
 #include "common.hpp"
 #include "epilogue.hpp"
 
@@ -121,6 +123,9 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     a.act = p.act;
     const int64_t blocks = (a.total + 255) / 256;
     if (blocks >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
+    if (debug_enabled())
+        fprintf(stderr, "cliffconv: conv_direct k=%d d_filter=%d, %lld workgroups of 256\n", KD,
+                (int)p.d_filter, (long long)blocks);
     hipLaunchKernelGGL((conv_direct_kernel<KD, NB>), dim3((unsigned)blocks), dim3(256), 0,
                        stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

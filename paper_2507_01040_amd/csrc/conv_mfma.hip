@@ -30,6 +30,8 @@
 //     [row][half][x][4] for N_B = 8 so that a fragment read is 64 consecutive
 //     words);
 //   * the raw filters [co][tap][blade] of this stage (no expansion).
+#include <stdio.h>
+
 #include <algorithm>
 #include <type_traits>
 
@@ -442,6 +444,12 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     a.stage_floats = (int)stage_floats;
     a.sign = p.sign;
     a.act = p.act;
+    if (debug_enabled())
+        fprintf(stderr,
+                "cliffconv: conv_mfma k=%d d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
+                "(%d channels x %d positions), %lld workgroups, %d channels/stage, %lld LDS bytes\n",
+                KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
+                (long long)lds_bytes);
     hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
