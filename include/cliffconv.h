@@ -93,8 +93,8 @@ typedef struct {
  * where * is the geometric product with the filter on the left, and
  * p ranges over [0, d_out)^k with d_out = d_image - d_filter + 1.
  *
- *   k         1, 2 or 3 (N_B = 2^k).  k = 2 and 3 run on the matrix cores;
- *             k = 1 runs on a plain per-output kernel.
+ *   k         1, 2 or 3 (N_B = 2^k), all on the matrix cores (shapes whose
+ *             staging does not fit fall back to a per-output kernel).
  *   g         host int8[k], each in {-1, 0, +1}, not all 0
  *   input     device [B, C_in, d_image^k, N_B]
  *   filters   device [C_in, C_out, d_filter^k, N_B]
@@ -118,14 +118,16 @@ cliff_status clifford_conv_nd(int k, const int8_t* g, int64_t B, int64_t C_in,
 typedef enum {
     CLIFF_ALGO_AUTO = 0,        /* what clifford_conv_nd does */
     CLIFF_ALGO_DIRECT = 1,      /* one thread per output multivector, fp32 FMA */
-    CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA (k = 2, 3 only),
-                                   tile shape chosen from the problem size */
-    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=2; 32 x 256 when
-                                   C_out <= 32) / 16 (k=3) channels x 128
-                                   positions per workgroup */
-    CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 32 channels x 32 positions */
-    CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 4 channels x 256 positions */
-    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 4 / 2 channels x 32 positions, one wave */
+    CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA, tile shape chosen
+                                   from the problem size */
+    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=1; k=2, or
+                                   32 x 256 when C_out <= 32) / 16 (k=3)
+                                   channels x 128 positions per workgroup */
+    CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32
+                                   positions */
+    CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 8 / 4 channels x 256 positions */
+    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 8 / 4 / 2 channels x 32 positions,
+                                   one wave */
 } cliff_algo;
 
 /*
@@ -148,7 +150,7 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
  *   output[b, co] = act( sum_{ci} weight[ci, co] * input[b, ci] + bias[co] )
  *
  * with the weight on the left of the geometric product.
- *   k, g      as for clifford_conv_nd (k = 1 runs on the per-output kernel)
+ *   k, g      as for clifford_conv_nd
  *   input     device [B, C_in, N_B]
  *   weight    device [C_in, C_out, N_B]
  *   bias      device [C_out, N_B], or NULL for zero

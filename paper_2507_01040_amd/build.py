@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcliffconv.so")
-SOURCES = ["api.cpp", "conv_mfma.hip", "conv_direct.hip", "act.hip"]
+SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -180,7 +180,6 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
                     overlaps(output, out_bytes, act->bias, C_out * 4))))
         return CLIFF_EOVERLAP;
     const bool mfma_forced = algo >= CLIFF_ALGO_MFMA;
-    if (mfma_forced && k == 1) return CLIFF_EUNSUPPORTED;
     if (B == 0) return CLIFF_OK;
 
     int8_t src[64], sign[64];
@@ -204,10 +203,8 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
     hipStream_t st = (hipStream_t)stream;
 
     if (algo == CLIFF_ALGO_DIRECT) return launch_conv_direct(p, st);
-    if (k >= 2) {
-        const cliff_status s = launch_conv_mfma(p, st);
-        if (s != CLIFF_EUNSUPPORTED || mfma_forced) return s;
-    }
+    const cliff_status s = k == 1 ? launch_conv1d_mfma(p, st) : launch_conv_mfma(p, st);
+    if (s != CLIFF_EUNSUPPORTED || mfma_forced) return s;
     return launch_conv_direct(p, st);
 }
 

@@ -65,6 +65,8 @@ bool debug_enabled();
 cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
 // Returns CLIFF_EUNSUPPORTED without launching when no MFMA tiling fits.
 cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream);
+// k = 1 on the matrix cores; CLIFF_EUNSUPPORTED without launching likewise.
+cliff_status launch_conv1d_mfma(const ConvProblem& p, hipStream_t stream);
 cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P,
                         const ActParams& a, const float* x, float* y,
                         hipStream_t stream);

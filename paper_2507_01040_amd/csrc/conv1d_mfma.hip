@@ -1,0 +1,373 @@
+// 1-D Clifford convolution (paper, Algorithm 1 with k = 1, N_B = 2) as an
+// implicit GEMM on the fp32 matrix cores (v_mfma_f32_16x16x4_f32).
+//
+// With two blades per multivector, one MFMA K-group of 4 covers two input
+// channels x two blades:
+//   A (16x4): rows = 8 output channels x 2 blades (co, i); column k = (c, j)
+//             with c = k / 2 the channel of the current pair and j = k % 2 the
+//             input blade.  Lane (row, k) reads the raw filter blade src(i, j)
+//             and applies the table's sign: the expanded Clifford kernel is
+//             never stored.
+//   B (4x16): the same (c, j) by 16 output positions.
+//   D (16x16): a lane ends with the two blades of two consecutive output
+//             channels at one position -> 8-byte stores, blade-last layout.
+// Output positions are flattened over (batch entry, x), so short signals (the
+// paper's 1-D layers have d_image = 60) still fill whole tiles.  A workgroup
+// owns P consecutive flattened positions and CO_WG output channels.  Its input
+// window is the contiguous run of (entry, x) positions from its first output
+// position to its last one plus d_filter - 1, crossing entry boundaries; the
+// positions of an entry past d_out are staged too (they are the last taps of
+// that entry).  Per stage (a group of input channels, double-buffered in LDS)
+// it stages each channel's window and raw filters with 4-byte direct
+// global->LDS loads, which need no alignment (a 1-D row or filter chunk is in
+// general not 16-byte aligned).
+#include <stdio.h>
+
+#include <algorithm>
+
+#include "common.hpp"
+#include "epilogue.hpp"
+
+namespace cliff {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+struct C1Args {
+    const float* x;
+    const float* w;
+    const float* bias;
+    float* y;
+    int C_in, C_out, D, Do, df;
+    int M;          // B * d_out flattened output positions
+    int n_co_blk;
+    int n_blk;
+    int cc;         // input channels per stage
+    int ccp;        // channel slots per stage buffer: cc rounded up to even
+    int n_stage;
+    int span2;      // floats per channel window: 2 * (P + rows_max * (d_filter - 1))
+    int stage_floats;
+    SignMasks sign;
+    ActParams act;
+};
+
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES>
+__global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1Args a)
+{
+    constexpr int NB = 2;
+    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int CPT = 8;  // output channels per 16-row tile
+    constexpr int CO_WG = WCO * MW * CPT;
+    constexpr int P = WPOS * NW * 16;
+
+    extern __shared__ f4 smem4[];
+    float* smem = reinterpret_cast<float*>(smem4);
+
+    const int df = DF > 0 ? DF : a.df;
+    const int D = a.D, Do = a.Do;
+    const int tid = threadIdx.x;
+
+    // XCD-aware renumbering: consecutive tiles (which share input) go to the
+    // same XCD and its L2.
+    const int bid = blockIdx.x;
+    const int per = a.n_blk / 8, rem = a.n_blk % 8;
+    const int xcd = bid % 8, slot = bid / 8;
+    const int tile = xcd < rem ? xcd * (per + 1) + slot
+                               : rem * (per + 1) + (xcd - rem) * per + slot;
+    const int co_blk = tile % a.n_co_blk;
+    const int m0 = (tile / a.n_co_blk) * P;
+    const int m_end = min(m0 + P, a.M);
+    const int co0 = co_blk * CO_WG;
+    const int b0 = m0 / Do;
+    const int x_first = m0 - b0 * Do;
+    const int b1 = (m_end - 1) / Do;
+    // window length in positions: (b1 - b0) D + x_last + d_filter - x_first
+    const int span = (b1 - b0) * D + (m_end - 1 - b1 * Do) + df - x_first;
+
+    // Stage buffer (floats): ccp channel windows [ccp][span2], then ccp
+    // channels of filters [ccp][co][tap][2].  Input slot t of this lane is
+    // window float f = t * NT + tid, filter slot t is filter float
+    // f = t * NT + tid (4-byte direct loads: lane i lands at base + 4 i).  The
+    // slots keep 32-bit byte offsets from the stage's uniform base pointers.
+    const int span2 = a.span2;
+    const int wch = CO_WG * df * NB;  // floats per channel of filters
+    const int w_lds = a.ccp * span2;
+    uint32_t xoffb[SIN], woffb[SW];
+#pragma unroll
+    for (int t = 0; t < SIN; ++t) {
+        const int f = t * NT + tid;
+        const int c_l = f / span2;
+        const int r = f - c_l * span2;
+        const int v = x_first + min(r / NB, span - 1);  // past the window: unused
+        const int bb = v / D;
+        xoffb[t] = 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
+    }
+#pragma unroll
+    for (int t = 0; t < SW; ++t) {
+        const int e = t * NT + tid;
+        const int c_l = e / wch;
+        const int e2 = e - c_l * wch;
+        const int co_l = e2 / (df * NB);
+        const int r = e2 - co_l * (df * NB);
+        const int co = min(co0 + co_l, a.C_out - 1);  // past C_out: unused
+        woffb[t] = 4u * (uint32_t)(c_l * a.C_out * df * NB + (co - co0) * df * NB + r);
+    }
+    const char* xbase = reinterpret_cast<const char*>(a.x + (int64_t)b0 * a.C_in * D * NB);
+    const char* wbase = reinterpret_cast<const char*>(a.w + (int64_t)co0 * df * NB);
+    const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
+    auto stage_channels = [&](int s) { return min(a.cc, a.C_in - s * a.cc); };
+    auto load_stage = [&](int s, int buf) {
+        const int ci0 = s * a.cc;
+        const int nv = stage_channels(s);
+        const char* xs = xbase + (int64_t)ci0 * D * NB * 4;
+        const char* ws = wbase + (int64_t)ci0 * a.C_out * df * NB * 4;
+        float* lx = smem + buf * a.stage_floats + wave_u * 64;
+        float* lw = lx + w_lds;
+#pragma unroll
+        for (int t = 0; t < SIN; ++t) {
+            if (t * NT + tid < nv * span2)
+                __builtin_amdgcn_global_load_lds(
+                    xs + xoffb[t], (__attribute__((address_space(3))) void*)(lx + t * NT), 4, 0, 0);
+        }
+#pragma unroll
+        for (int t = 0; t < SW; ++t) {
+            if (t * NT + tid < nv * wch)
+                __builtin_amdgcn_global_load_lds(
+                    ws + woffb[t], (__attribute__((address_space(3))) void*)(lw + t * NT), 4, 0, 0);
+        }
+    };
+
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wco = wave % WCO;
+    const int wpos = wave / WCO;
+    const int mrow = lane & 15;
+    const int kk = lane >> 4;
+    const int c_sub = kk >> 1;  // channel of the pair
+    const int j = kk & 1;       // input blade
+
+    // A: row mrow = (output channel co_a, blade i_a), column (c_sub, j)
+    const int co_a = mrow >> 1;
+    const int i_a = mrow & 1;
+    const float sg = sign_of(a.sign, i_a * NB + j);
+    const int wofs =
+        w_lds + c_sub * wch + (wco * MW * CPT + co_a) * df * NB + src_blade(NB, i_a, j);
+    // B: row (c_sub, j), column mrow = output position
+    int xoff[NW];
+#pragma unroll
+    for (int nw = 0; nw < NW; ++nw) {
+        // tail lanes read a valid position; their outputs are not stored
+        const int m = min(m0 + (wpos * NW + nw) * 16 + mrow, m_end - 1);
+        const int bb = m / Do;
+        xoff[nw] = c_sub * span2 + ((bb - b0) * D + (m - bb * Do) - x_first) * NB + j;
+    }
+
+    f4 acc[MW][NW];
+#pragma unroll
+    for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+        for (int nw = 0; nw < NW; ++nw) acc[mw][nw] = f4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](int buf, int nv) {
+        const float* S0 = smem + buf * a.stage_floats;
+        for (int c_l = 0; c_l < nv; c_l += 2) {
+            // the second channel of a pair past nv contributes zero (its LDS
+            // slot holds stale data: selected away, never multiplied)
+            const bool on = c_l + c_sub < nv;
+            const float* S = S0 + c_l * span2;
+            const float* Sw = S0 + c_l * wch;
+            auto step = [&](int tap) {
+                float av[MW], bv[NW];
+#pragma unroll
+                for (int mw = 0; mw < MW; ++mw) {
+                    const float v = Sw[wofs + mw * CPT * df * NB + tap * NB];
+                    av[mw] = on ? v * sg : 0.f;
+                }
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw) {
+                    const float v = S[xoff[nw] + tap * NB];
+                    bv[nw] = on ? v : 0.f;
+                }
+#pragma unroll
+                for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                    for (int nw = 0; nw < NW; ++nw)
+                        acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            av[mw], bv[nw], acc[mw][nw], 0, 0, 0);
+            };
+            if constexpr (DF > 0) {
+#pragma unroll
+                for (int tap = 0; tap < DF; ++tap) step(tap);
+            } else {
+                for (int tap = 0; tap < df; ++tap) step(tap);
+            }
+        }
+    };
+
+    load_stage(0, 0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int s = 0; s < a.n_stage; ++s) {
+        // buffer (s+1)&1 was last read in iteration s-1, before its barrier
+        if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
+        compute(s & 1, stage_channels(s));
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+    }
+
+    // Epilogue: lane row 4 kk + r is channel 2 kk + r / 2, blade r % 2.
+    const bool has_act = a.act.mode >= 0;
+    int gslot0 = -1, gslot1 = -1;
+    if (has_act) {
+        gslot0 = gate_slot(a.act, 0);
+        gslot1 = gate_slot(a.act, 1);
+    }
+    int64_t ybase[NW];
+    bool mvalid[NW];
+#pragma unroll
+    for (int nw = 0; nw < NW; ++nw) {
+        const int m = m0 + (wpos * NW + nw) * 16 + mrow;
+        mvalid[nw] = m < m_end;
+        const int bb = m / Do;
+        ybase[nw] = ((int64_t)bb * a.C_out * Do + (m - bb * Do)) * NB;
+    }
+#pragma unroll
+    for (int mw = 0; mw < MW; ++mw) {
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int co = co0 + (wco * MW + mw) * CPT + 2 * kk + half;
+            const bool cvalid = co < a.C_out;
+            float bias0 = 0.f, bias1 = 0.f, cf0 = 0.f, cf1 = 0.f;
+            if (cvalid && a.bias) {
+                bias0 = a.bias[co * NB];
+                bias1 = a.bias[co * NB + 1];
+            }
+            if (has_act && cvalid) {
+                cf0 = gate_coef(a.act, gslot0, co);
+                cf1 = gate_coef(a.act, gslot1, co);
+            }
+#pragma unroll
+            for (int nw = 0; nw < NW; ++nw) {
+                float v0 = acc[mw][nw][2 * half] + bias0;
+                float v1 = acc[mw][nw][2 * half + 1] + bias1;
+                if (has_act && cvalid) {
+                    const float g = gate_sigmoid(a.act, cf0 * v0 + cf1 * v1, co);
+                    v0 *= g;
+                    v1 *= g;
+                }
+                if (cvalid && mvalid[nw]) {
+                    float* yp = a.y + ybase[nw] + (int64_t)co * Do * NB;
+                    *reinterpret_cast<float2*>(yp) = make_float2(v0, v1);
+                }
+            }
+        }
+    }
+}
+
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES>
+cliff_status run1d(const ConvProblem& p, hipStream_t stream)
+{
+    constexpr int NB = 2;
+    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int CO_WG = WCO * MW * 8;
+    constexpr int P = WPOS * NW * 16;
+    const int64_t D = p.d_image, Do = p.d_out, df = p.d_filter;
+    const int64_t M = p.B * Do;
+    const int64_t n_pblk = (M + P - 1) / P;
+    const int64_t n_co_blk = (p.C_out + CO_WG - 1) / CO_WG;
+    const int64_t n_blk = n_pblk * n_co_blk;
+    // P consecutive flattened positions touch at most rows_max batch entries
+    const int64_t rows_max = std::min<int64_t>(p.B, (P + Do - 2) / Do + 1);
+    const int64_t span_max = P + rows_max * (df - 1);
+    const int64_t ch_floats = span_max * NB + CO_WG * df * NB;
+    // LDS: two stage buffers per workgroup, WAVES waves per SIMD resident
+    const int64_t wg_per_cu = std::max<int64_t>(1, 4 * WAVES / (WCO * WPOS));
+    const int64_t lds_budget = std::min<int64_t>(64 * 1024, 160 * 1024 / wg_per_cu);
+    const int64_t mfma_per_pair = df * MW * NW;
+    int64_t ccp = 2 * std::max<int64_t>(1, (512 + mfma_per_pair - 1) / mfma_per_pair);
+    ccp = std::min<int64_t>(ccp, (lds_budget / (2 * ch_floats * 4)) & ~int64_t(1));
+    ccp = std::min<int64_t>(ccp, ((int64_t)SIN * NT / (span_max * NB)) & ~int64_t(1));
+    ccp = std::min<int64_t>(ccp, ((int64_t)SW * NT / (CO_WG * df * NB)) & ~int64_t(1));
+    ccp = std::min<int64_t>(ccp, (p.C_in + 1) & ~int64_t(1));
+    if (ccp < 2 || M >= (1ll << 31) || n_blk >= (1ll << 31) ||
+        rows_max * p.C_in * D * NB >= (1ll << 30) || ccp * p.C_out * df * NB >= (1ll << 30))
+        return CLIFF_EUNSUPPORTED;
+    const int64_t cc = std::min<int64_t>(ccp, p.C_in);
+    const int64_t stage_floats = ccp * ch_floats;
+    const int64_t lds_bytes = 2 * stage_floats * 4;
+
+    C1Args a;
+    a.x = p.x;
+    a.w = p.w;
+    a.bias = p.bias;
+    a.y = p.y;
+    a.C_in = (int)p.C_in;
+    a.C_out = (int)p.C_out;
+    a.D = (int)D;
+    a.Do = (int)Do;
+    a.df = (int)df;
+    a.M = (int)M;
+    a.n_co_blk = (int)n_co_blk;
+    a.n_blk = (int)n_blk;
+    a.cc = (int)cc;
+    a.ccp = (int)ccp;
+    a.n_stage = (int)((p.C_in + cc - 1) / cc);
+    a.span2 = (int)(span_max * NB);
+    a.stage_floats = (int)stage_floats;
+    a.sign = p.sign;
+    a.act = p.act;
+    if (debug_enabled())
+        fprintf(stderr,
+                "cliffconv: conv1d_mfma d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
+                "(%d channels x %d positions), %lld workgroups, %d channels/stage, "
+                "%lld LDS bytes\n",
+                (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
+                (long long)lds_bytes);
+    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES>),
+                       dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
+    return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
+}
+
+// Tile shapes (waves along channels x waves along positions, MFMA tiles per
+// wave along channels x along positions):
+//   wide   2x2 waves of 4x4 tiles: 64 channels x 128 positions
+//   medium 2x1 waves of 4x2 tiles: 64 channels x  32 positions
+//   narrow 1x4 waves of 1x4 tiles:  8 channels x 256 positions
+//   tiny   one wave of 1x2 tiles:   8 channels x  32 positions
+template <int DF>
+cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
+{
+    // <DF, WCO, WPOS, MW, NW, input slots, filter slots, waves per SIMD>
+    auto wide = [&] { return run1d<DF, 2, 2, 4, 4, 8, 18, 2>(p, stream); };
+    auto medium = [&] { return run1d<DF, 2, 1, 4, 2, 8, 18, 2>(p, stream); };
+    auto narrow = [&] { return run1d<DF, 1, 4, 1, 4, 16, 4, 2>(p, stream); };
+    auto tiny = [&] { return run1d<DF, 1, 1, 1, 2, 12, 12, 4>(p, stream); };
+    switch (p.mfma_shape) {
+    case 0: return wide();
+    case 1: return medium();
+    case 2: return narrow();
+    case 3: return tiny();
+    default: break;
+    }
+    const int64_t M = p.B * p.d_out;
+    auto blocks = [&](int64_t co_wg, int64_t pos) {
+        return ((M + pos - 1) / pos) * ((p.C_out + co_wg - 1) / co_wg);
+    };
+    cliff_status s = CLIFF_EUNSUPPORTED;
+    if (p.C_out > 32 && blocks(64, 128) >= 256) s = wide();
+    if (s == CLIFF_EUNSUPPORTED && p.C_out > 32 && blocks(64, 32) >= 256) s = medium();
+    if (s == CLIFF_EUNSUPPORTED && blocks(8, 256) >= 128) s = narrow();
+    if (s == CLIFF_EUNSUPPORTED) s = tiny();
+    return s;
+}
+
+}  // namespace
+
+cliff_status launch_conv1d_mfma(const ConvProblem& p, hipStream_t stream)
+{
+    if (p.k != 1) return CLIFF_EUNSUPPORTED;
+    if (p.d_filter == 3) return run1d_shape<3>(p, stream);
+    return run1d_shape<0>(p, stream);
+}
+
+}  // namespace cliff

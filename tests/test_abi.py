@@ -167,10 +167,12 @@ def test_standalone_act_shape_and_pointer_errors(no_gpu):
     assert lib.multivector_act(4, 2, 3, 5, None, FAKE, FAKE + (1 << 24), None) == P.CLIFF_EINVAL
 
 
-def test_mfma_rejects_k1(no_gpu):
-    st = P.clifford_conv_nd_algo(1, (-1,), 2, 3, 4, 8, 3, FAKE, FAKE + (1 << 24),
+def test_forced_tile_refuses_unstageable_k1(no_gpu):
+    # the 1-D medium tile (64 channels) cannot stage 64 x 17 filter taps per
+    # channel pair: refused before any launch
+    st = P.clifford_conv_nd_algo(1, (-1,), 2, 3, 64, 60, 17, FAKE, FAKE + (1 << 24),
                                  FAKE + (2 << 24), FAKE + (3 << 24), None, 0,
-                                 P.ALGO_MFMA)
+                                 P.ALGO_MFMA_MEDIUM)
     assert st == P.CLIFF_EUNSUPPORTED
 
 

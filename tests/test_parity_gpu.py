@@ -46,6 +46,18 @@ SHAPES3 = [
     (8, 4, 4, 16, 3),     # several channels per stage
     (64, 37, 64, 1, 1),   # linear layer
 ]
+SHAPES1 = [
+    (1, 1, 1, 3, 3),      # one output, one channel (odd: half of the pair is off)
+    (2, 5, 3, 17, 3),     # odd channels, C_out < tile
+    (3, 4, 20, 60, 17),   # the paper's 1-D signal and filter lengths
+    (4, 3, 65, 60, 17),   # two channel blocks of the wide tile
+    (5, 7, 9, 10, 1),     # pointwise
+    (2, 70, 70, 300, 3),  # several stages, partial last stage, long signal
+    (9, 3, 5, 4, 4),      # d_out = 1: each tile spans many batch entries
+    (1, 2, 8, 200, 5),
+    (6, 39, 19, 80, 4),   # even filter, odd channel count over stages
+    (64, 37, 64, 1, 1),   # linear layer
+]
 
 
 def _case(seed, g, shape):
@@ -92,9 +104,32 @@ def test_conv3d_parity(algo, shape):
     assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(shape))
 
 
-@pytest.mark.parametrize("g", SIG2 + SIG3, ids=str)
+@pytest.mark.parametrize("algo", ALGOS, ids=ALGO_IDS)
+@pytest.mark.parametrize("shape", SHAPES1, ids=str)
+def test_conv1d_parity(algo, shape):
+    g = (-1,)
+    s, x, f, b = _case(114, g, shape)
+    y = _run_allow_unsupported(g, x, f, b, algo)
+    if y is None:
+        return
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(shape))
+
+
+def test_conv1d_paper_shape_runs_on_mfma():
+    # the paper's 1-D layer (d_image 60, d_filter 17) must take the matrix-core path
+    g = (1,)
+    s, x, f, b = _case(115, g, (16, 16, 16, 60, 17))
+    for algo in (P.ALGO_MFMA, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY):
+        assert_parity(gpu_conv(g, x, f, b, algo=algo), oracle.conv_nd(x, f, b, g),
+                      what="algo %d" % algo)
+
+
+SIG1 = [(-1,), (1,)]
+
+
+@pytest.mark.parametrize("g", SIG1 + SIG2 + SIG3, ids=str)
 def test_all_signatures(g):
-    shape = (2, 3, 6, 9, 3) if len(g) == 2 else (2, 3, 3, 6, 3)
+    shape = {1: (2, 3, 6, 20, 3), 2: (2, 3, 6, 9, 3), 3: (2, 3, 3, 6, 3)}[len(g)]
     s, x, f, b = _case(102, g, shape)
     ref = oracle.conv_nd(x, f, b, g)
     for algo in (P.ALGO_MFMA, P.ALGO_DIRECT, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_TINY):
@@ -149,6 +184,23 @@ def test_fused_act_2d(algo, mode, blades):
     g = (1, -1)
     s, x, f, b = _case(106, g, (3, 5, 70, 12, 3))
     aw, ab = _act_args(5, 70, mode, blades)
+    y = _run_allow_unsupported(g, x, f, b, algo, act=(mode, blades, aw, ab))
+    if y is None:
+        return
+    ref = oracle.act(oracle.conv_nd(x, f, b, g), mode, blades, aw, ab)
+    assert_parity(y, ref)
+
+
+ACTS1 = [(AGG_LINEAR, (0, 1)), (AGG_SUM, (0, 1)), (AGG_MEAN, (1, 0)), (AGG_LINEAR, (1,)),
+         (AGG_MEAN, (0,))]
+
+
+@pytest.mark.parametrize("algo", FUSED_ALGOS, ids=FUSED_IDS)
+@pytest.mark.parametrize("mode,blades", ACTS1, ids=str)
+def test_fused_act_1d(algo, mode, blades):
+    g = (-1,)
+    s, x, f, b = _case(116, g, (3, 5, 70, 50, 5))
+    aw, ab = _act_args(9, 70, mode, blades)
     y = _run_allow_unsupported(g, x, f, b, algo, act=(mode, blades, aw, ab))
     if y is None:
         return
