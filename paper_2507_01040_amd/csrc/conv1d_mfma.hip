@@ -24,9 +24,17 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "common.hpp"
 #include "epilogue.hpp"
+
+#ifndef CLIFF_LDS1  // LDS bytes per workgroup at most (two stage buffers)
+#define CLIFF_LDS1 (64 * 1024)
+#endif
+#ifndef CLIFF_W1  // wide tile: WCO, WPOS, MW, NW, input slots, filter slots, waves/SIMD
+#define CLIFF_W1 2, 2, 4, 4, 8, 18, 2
+#endif
 
 namespace cliff {
 namespace {
@@ -168,40 +176,64 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
 #pragma unroll
         for (int nw = 0; nw < NW; ++nw) acc[mw][nw] = f4{0.f, 0.f, 0.f, 0.f};
 
+    // One channel pair: all taps.  MASKED: the pair's second channel does not
+    // exist (odd channel count in the stage); its LDS slot holds stale data,
+    // which is selected away (never multiplied, so stale NaN/Inf cannot leak).
+    auto pair = [&](const float* S0, int c_l, auto masked) {
+        constexpr bool MASKED = decltype(masked)::value;
+        const bool on = !MASKED || c_sub == 0;
+        const float* S = S0 + c_l * span2;
+        const float* Sw = S0 + c_l * wch;
+        float ar[MW], br[NW];  // raw fragments of the next tap
+        auto read = [&](int tap) {
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw) ar[mw] = Sw[wofs + mw * CPT * df * NB + tap * NB];
+#pragma unroll
+            for (int nw = 0; nw < NW; ++nw) br[nw] = S[xoff[nw] + tap * NB];
+        };
+        auto step = [&](int tap, bool prefetch) {
+            float av[MW], bv[NW];
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw) av[mw] = ar[mw];
+#pragma unroll
+            for (int nw = 0; nw < NW; ++nw) bv[nw] = br[nw];
+            if constexpr (DF > 0) {
+                // software pipelining: the reads of tap + 1 are issued before
+                // this tap's MFMAs (measured faster with the taps unrolled,
+                // slower with a runtime tap loop)
+                if (prefetch) read(tap + 1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw) av[mw] = MASKED && !on ? 0.f : av[mw] * sg;
+            if constexpr (MASKED) {
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw) bv[nw] = on ? bv[nw] : 0.f;
+            }
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw)
+                    acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mw], bv[nw],
+                                                                        acc[mw][nw], 0, 0, 0);
+            if constexpr (DF > 0)
+                __builtin_amdgcn_sched_barrier(0);
+            else if (prefetch)
+                read(tap + 1);
+        };
+        read(0);
+        if constexpr (DF > 0) {
+#pragma unroll
+            for (int tap = 0; tap < DF; ++tap) step(tap, tap + 1 < DF);
+        } else {
+            for (int tap = 0; tap < df; ++tap) step(tap, tap + 1 < df);
+        }
+    };
     auto compute = [&](int buf, int nv) {
         const float* S0 = smem + buf * a.stage_floats;
-        for (int c_l = 0; c_l < nv; c_l += 2) {
-            // the second channel of a pair past nv contributes zero (its LDS
-            // slot holds stale data: selected away, never multiplied)
-            const bool on = c_l + c_sub < nv;
-            const float* S = S0 + c_l * span2;
-            const float* Sw = S0 + c_l * wch;
-            auto step = [&](int tap) {
-                float av[MW], bv[NW];
-#pragma unroll
-                for (int mw = 0; mw < MW; ++mw) {
-                    const float v = Sw[wofs + mw * CPT * df * NB + tap * NB];
-                    av[mw] = on ? v * sg : 0.f;
-                }
-#pragma unroll
-                for (int nw = 0; nw < NW; ++nw) {
-                    const float v = S[xoff[nw] + tap * NB];
-                    bv[nw] = on ? v : 0.f;
-                }
-#pragma unroll
-                for (int mw = 0; mw < MW; ++mw)
-#pragma unroll
-                    for (int nw = 0; nw < NW; ++nw)
-                        acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            av[mw], bv[nw], acc[mw][nw], 0, 0, 0);
-            };
-            if constexpr (DF > 0) {
-#pragma unroll
-                for (int tap = 0; tap < DF; ++tap) step(tap);
-            } else {
-                for (int tap = 0; tap < df; ++tap) step(tap);
-            }
-        }
+        const int nfull = nv & ~1;
+        for (int c_l = 0; c_l < nfull; c_l += 2) pair(S0, c_l, std::false_type{});
+        if (nv & 1) pair(S0, nfull, std::true_type{});
     };
 
     load_stage(0, 0);
@@ -282,7 +314,7 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     const int64_t ch_floats = span_max * NB + CO_WG * df * NB;
     // LDS: two stage buffers per workgroup, WAVES waves per SIMD resident
     const int64_t wg_per_cu = std::max<int64_t>(1, 4 * WAVES / (WCO * WPOS));
-    const int64_t lds_budget = std::min<int64_t>(64 * 1024, 160 * 1024 / wg_per_cu);
+    const int64_t lds_budget = std::min<int64_t>(CLIFF_LDS1, 160 * 1024 / wg_per_cu);
     const int64_t mfma_per_pair = df * MW * NW;
     int64_t ccp = 2 * std::max<int64_t>(1, (512 + mfma_per_pair - 1) / mfma_per_pair);
     ccp = std::min<int64_t>(ccp, (lds_budget / (2 * ch_floats * 4)) & ~int64_t(1));
@@ -338,7 +370,7 @@ template <int DF>
 cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
 {
     // <DF, WCO, WPOS, MW, NW, input slots, filter slots, waves per SIMD>
-    auto wide = [&] { return run1d<DF, 2, 2, 4, 4, 8, 18, 2>(p, stream); };
+    auto wide = [&] { return run1d<DF, CLIFF_W1>(p, stream); };
     auto medium = [&] { return run1d<DF, 2, 1, 4, 2, 8, 18, 2>(p, stream); };
     auto narrow = [&] { return run1d<DF, 1, 4, 1, 4, 16, 4, 2>(p, stream); };
     auto tiny = [&] { return run1d<DF, 1, 1, 1, 2, 12, 12, 4>(p, stream); };
@@ -355,9 +387,8 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     };
     cliff_status s = CLIFF_EUNSUPPORTED;
     if (p.C_out > 32 && blocks(64, 128) >= 256) s = wide();
-    if (s == CLIFF_EUNSUPPORTED && p.C_out > 32 && blocks(64, 32) >= 256) s = medium();
-    if (s == CLIFF_EUNSUPPORTED && blocks(8, 256) >= 128) s = narrow();
     if (s == CLIFF_EUNSUPPORTED) s = tiny();
+    if (s == CLIFF_EUNSUPPORTED) s = narrow();
     return s;
 }
 
@@ -366,7 +397,9 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
 cliff_status launch_conv1d_mfma(const ConvProblem& p, hipStream_t stream)
 {
     if (p.k != 1) return CLIFF_EUNSUPPORTED;
+    // the filter lengths of the paper's layers get unrolled tap loops
     if (p.d_filter == 3) return run1d_shape<3>(p, stream);
+    if (p.d_filter == 17) return run1d_shape<17>(p, stream);
     return run1d_shape<0>(p, stream);
 }
 

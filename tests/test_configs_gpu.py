@@ -1,4 +1,4 @@
-"""Full-size parity on the five benchmark workloads, run through the C ABI in
+"""Full-size parity on the benchmark workloads, run through the C ABI in
 the launch configuration the benchmark times (clifford_conv_nd, automatic
 kernel choice, activation fused into the convolution for the blocks).
 
@@ -71,7 +71,7 @@ def test_c1_full():
     assert_parity(y, ref)
 
 
-@pytest.mark.parametrize("name", ["conv2d_c64_d128", "conv3d_c32_d32"])
+@pytest.mark.parametrize("name", ["conv2d_c64_d128", "conv3d_c32_d32", "conv1d_c64_d60"])
 def test_single_conv_sampled(name):
     w = W.WORKLOADS[name]
     x, ps = W.make_inputs(w)

@@ -112,7 +112,7 @@ def _fan_bound(C_in, d_filter, k):
     return 1.0 / math.sqrt(C_in * d_filter ** k)
 
 
-# The five workloads the benchmark and the full-size parity tests use.
+# The workloads the benchmark and the full-size parity tests use.
 WORKLOADS = {
     "conv2d_c4_d16": Workload(
         "conv2d_c4_d16", 1000,
@@ -136,6 +136,11 @@ WORKLOADS = {
         _conv_layers(3, (1, 1, 1), 8, 64, 36, 3, 2),
         (ActSpec(AGG_MEAN, tuple(range(8))), ActSpec(AGG_MEAN, tuple(range(8)))),
         (_fan_bound(64, 3, 3),) * 2, bias_std=0.1),
+    # the paper's 1-D layer (d_image 60, d_filter 17) at a GPU-sized batch
+    "conv1d_c64_d60": Workload(
+        "conv1d_c64_d60", 1005,
+        _conv_layers(1, (-1,), 4096, 64, 60, 17, 1), (None,),
+        (_fan_bound(64, 17, 1),), bias_std=0.1),
 }
 WORKLOAD_ORDER = list(WORKLOADS)
 
