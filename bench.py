@@ -130,8 +130,9 @@ class Runner:
             self.step([ev[s][l] for l in range(n_l)])
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        per_layer_ms = [float(np.mean([ev[s][l][0].elapsed_time(ev[s][l][1])
-                                       for s in range(steps)])) for l in range(n_l)]
+        self.last_samples = [[ev[s][l][0].elapsed_time(ev[s][l][1]) for s in range(steps)]
+                             for l in range(n_l)]
+        per_layer_ms = [float(np.mean(v)) for v in self.last_samples]
         return wall / steps * 1e3, per_layer_ms
 
 
@@ -169,6 +170,10 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
     res = {"workload": name, "ms_per_step": round(ms, 4),
            "useful_gflops": round(flops / (ms * 1e-3) / 1e9, 1),
            "kernel_ms": [round(v, 4) for v in per_layer],
+           "kernel_ms_median_min_max": [[round(float(np.median(v)), 4), round(min(v), 4),
+                                         round(max(v), 4)] for v in r.last_samples],
+           "kernel_algorithmic_GB_s": [round(l.algorithmic_bytes() / (t * 1e-3) / 1e9, 1)
+                                       for l, t in zip(w.layers, per_layer)],
            "kernel_tflops": [round(l.useful_flops() / (t * 1e-3) / 1e12, 2)
                              for l, t in zip(w.layers, per_layer)]}
     res["frac_of_fp32_mfma_peak"] = round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
@@ -181,6 +186,58 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
         del plain
     del r
     return res
+
+
+def measure_mfma_peak(n_wg: int = 4096, iters: int = 1024, launches: int = 5):
+    """Sustained fp32 matrix-core throughput of this chip (the probe kernel:
+    independent MFMAs from registers, no memory traffic), best of several
+    launches timed with HIP events."""
+    import torch
+    import paper_2507_01040_amd as P
+    out = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda:0")
+    lib = P.load()
+    stream = torch.cuda.current_stream().cuda_stream
+    assert lib.cliffconv_mfma_peak_probe(n_wg, iters, out.data_ptr(), stream) == P.CLIFF_OK
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(launches)]
+    for e0, e1 in ev:
+        e0.record()
+        lib.cliffconv_mfma_peak_probe(n_wg, iters, out.data_ptr(), stream)
+        e1.record()
+    torch.cuda.synchronize()
+    ms = min(e0.elapsed_time(e1) for e0, e1 in ev)
+    flops = n_wg * 4 * iters * 16 * 2048
+    return {"tflops": round(flops / (ms * 1e-3) / 1e12, 2), "kernel_ms": round(ms, 4),
+            "frac_of_nominal": round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4),
+            "probe": "%d workgroups x 4 waves x %d x 16 independent v_mfma_f32_16x16x4_f32"
+                     % (n_wg, iters)}
+
+
+def cpu_baseline_1thread():
+    """The oracle on one thread, for the paper's single-core context: the 2D
+    tiny workload in full and a slice of the headline workload (batch entry
+    0, output channels 0..15)."""
+    import oracle
+    out = []
+    w = W.WORKLOADS["conv2d_c4_d16"]
+    x, ps = W.make_inputs(w)
+    t0 = time.perf_counter()
+    oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g, nthreads=1)
+    t = time.perf_counter() - t0
+    out.append({"workload": w.name, "sample": "full", "gflops": round(w.useful_flops / t / 1e9, 3),
+                "seconds": round(t, 3)})
+    w = W.WORKLOADS[HEADLINE]
+    x, ps = W.make_inputs(w)
+    s = w.layers[0]
+    f = np.ascontiguousarray(ps[0].filters[:, :16])
+    b = np.ascontiguousarray(ps[0].bias[:16])
+    t0 = time.perf_counter()
+    oracle.conv_nd(x[0:1], f, b, s.g, nthreads=1)
+    t = time.perf_counter() - t0
+    flops = s.useful_flops() // s.B // s.C_out * 16
+    out.append({"workload": w.name, "sample": "batch entry 0, output channels 0..15",
+                "gflops": round(flops / t / 1e9, 3), "seconds": round(t, 3)})
+    return out
 
 
 def measure_act(nb: int, B: int, C: int, Pn: int, mode: int, blades, steps: int = 20,
@@ -287,6 +344,7 @@ def main():
     w = W.WORKLOADS[args.workload]
     head = measure(args.workload, args.steps, args.warmup,
                    epilogue_overhead=not args.no_extra)
+    probe = None if args.no_extra else measure_mfma_peak()
     s0 = w.layers[0]
     dom = int(np.argmax(head["kernel_ms"]))
     dom_ms = head["kernel_ms"][dom]
@@ -318,7 +376,11 @@ def main():
                      "kernel": "conv_mfma_kernel (layer %d)" % dom,
                      "kernel_ms": dom_ms,
                      "kernel_source_hash": kernel_source_hash()},
+        "workload_detail": head,
     }
+    if probe is not None:
+        line["mfma_probe"] = probe
+        line["roofline"]["frac_of_mfma_probe"] = round(achieved / probe["tflops"], 4)
     if not args.no_extra:
         extra = {}
         for name in W.WORKLOAD_ORDER:
@@ -338,6 +400,8 @@ def main():
         ]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
+        if not args.no_extra:
+            line["cpu_baseline_1thread"] = cpu_baseline_1thread()
     print(json.dumps(line), flush=True)
 
 

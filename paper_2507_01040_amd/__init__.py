@@ -27,7 +27,8 @@ ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
 ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
 
 EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
-            "multivector_act", "cliffconv_cayley_table", "cliffconv_status_string")
+            "multivector_act", "cliffconv_cayley_table", "cliffconv_status_string",
+            "cliffconv_mfma_peak_probe")
 
 
 class CliffActDesc(ctypes.Structure):
@@ -65,10 +66,11 @@ def load(path: str = LIB_PATH):
     lib.multivector_act.argtypes = [i32, i64, i64, i64,
                                     ctypes.POINTER(CliffActDesc), vp, vp, vp]
     lib.cliffconv_cayley_table.argtypes = [i32, vp, vp, vp]
+    lib.cliffconv_mfma_peak_probe.argtypes = [i64, ctypes.c_int32, vp, vp]
     lib.cliffconv_status_string.argtypes = [i32]
     lib.cliffconv_status_string.restype = ctypes.c_char_p
     for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
-                 "multivector_act", "cliffconv_cayley_table"):
+                 "multivector_act", "cliffconv_cayley_table", "cliffconv_mfma_peak_probe"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcliffconv.so")
-SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip"]
+SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip",
+           "mfma_probe.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -27,11 +28,11 @@ FLAGS = [
 ]
 
 
-# Per-source device-compiler options: the matrix-core kernel is scheduled with
-# LLVM's iterative ILP strategy (measured faster than the default on gfx950).
-SOURCE_FLAGS = {
-    "conv_mfma.hip": ["-Xarch_device", "-mllvm=-amdgpu-sched-strategy=iterative-ilp"],
-}
+# Per-source device-compiler options (none at present: the matrix-core kernels
+# order their instructions with scheduling-group barriers, which LLVM's
+# default scheduler honours; the iterative-ILP strategy ignores them and was
+# measured 1-2 % slower with them).
+SOURCE_FLAGS = {}
 
 
 def _compile(src: str, extra) -> str:

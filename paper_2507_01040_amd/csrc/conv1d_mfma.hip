@@ -29,6 +29,9 @@
 #include "common.hpp"
 #include "epilogue.hpp"
 
+#ifndef CLIFF_SGB_IL  // MFMAs between two of the next step's LDS reads; 0: reads clumped
+#define CLIFF_SGB_IL 2
+#endif
 #ifndef CLIFF_LDS1  // LDS bytes per workgroup at most (two stage buffers)
 #define CLIFF_LDS1 (64 * 1024)
 #endif
@@ -202,7 +205,9 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
                 // this tap's MFMAs (measured faster with the taps unrolled,
                 // slower with a runtime tap loop)
                 if (prefetch) read(tap + 1);
+#if !CLIFF_SGB_IL
                 __builtin_amdgcn_sched_barrier(0);
+#endif
             }
 #pragma unroll
             for (int mw = 0; mw < MW; ++mw) av[mw] = MASKED && !on ? 0.f : av[mw] * sg;
@@ -216,10 +221,20 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
                 for (int nw = 0; nw < NW; ++nw)
                     acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mw], bv[nw],
                                                                         acc[mw][nw], 0, 0, 0);
-            if constexpr (DF > 0)
+            if constexpr (DF > 0) {
+#if CLIFF_SGB_IL
+                __builtin_amdgcn_sched_group_barrier(0x002, MW, 0);
+#pragma unroll
+                for (int r = 0; r < MW + NW; ++r) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, CLIFF_SGB_IL, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, MW * NW, 0);
+#endif
                 __builtin_amdgcn_sched_barrier(0);
-            else if (prefetch)
+            } else if (prefetch) {
                 read(tap + 1);
+            }
         };
         read(0);
         if constexpr (DF > 0) {

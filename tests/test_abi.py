@@ -1,7 +1,7 @@
 """Host-side tests of the C ABI (no kernel is ever launched here).
 
-* libcliffconv.so loads and exports every entry point include/cliffconv.h
-  declares;
+* libcliffconv.so loads and exports every entry point the headers in
+  include/ declare;
 * the library's signature-driven table (closed form on bitmasks) equals the
   oracle's word-rewriting table for all 39 signatures with k <= 3;
 * every argument error is reported before any device work.
@@ -11,6 +11,7 @@ carries a defect the library must reject; the module is skipped where a GPU
 is visible (the GPU suite checks the same errors with real buffers).
 """
 import ctypes
+import glob
 import itertools
 import os
 import re
@@ -21,7 +22,7 @@ import oracle
 import paper_2507_01040_amd as P
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "cliffconv.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def _lib_or_skip():
@@ -31,9 +32,11 @@ def _lib_or_skip():
 
 
 def _declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M))
+    return names
 
 
 def test_header_declares_the_entry_points():
@@ -174,6 +177,14 @@ def test_forced_tile_refuses_unstageable_k1(no_gpu):
                                  FAKE + (2 << 24), FAKE + (3 << 24), None, 0,
                                  P.ALGO_MFMA_MEDIUM)
     assert st == P.CLIFF_EUNSUPPORTED
+
+
+def test_mfma_probe_argument_errors(no_gpu):
+    lib = P.load()
+    assert lib.cliffconv_mfma_peak_probe(4, 8, None, None) == P.CLIFF_EINVAL
+    assert lib.cliffconv_mfma_peak_probe(0, 8, FAKE, None) == P.CLIFF_ESHAPE
+    assert lib.cliffconv_mfma_peak_probe(4, 0, FAKE, None) == P.CLIFF_ESHAPE
+    assert lib.cliffconv_mfma_peak_probe(1 << 31, 8, FAKE, None) == P.CLIFF_ESHAPE
 
 
 def test_bad_algo(no_gpu):
