@@ -35,8 +35,8 @@
 #ifndef CLIFF_LDS1  // LDS bytes per workgroup at most (two stage buffers)
 #define CLIFF_LDS1 (64 * 1024)
 #endif
-#ifndef CLIFF_W1  // wide tile: WCO, WPOS, MW, NW, input slots, filter slots, waves/SIMD
-#define CLIFF_W1 2, 2, 4, 4, 8, 18, 2
+#ifndef CLIFF_W1  // wide tile: WCO, WPOS, MW, NW, input slots
+#define CLIFF_W1 2, 2, 4, 4, 8
 #endif
 
 namespace cliff {
@@ -62,7 +62,7 @@ struct C1Args {
     ActParams act;
 };
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW>
 __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1Args a)
 {
     constexpr int NB = 2;
@@ -97,8 +97,11 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
 
     // Stage buffer (floats): ccp channel windows [ccp][span2], then ccp
     // channels of filters [ccp][co][tap][2].  Input slot t of this lane is
-    // window float f = t * NT + tid, filter slot t is filter float
-    // f = t * NT + tid (4-byte direct loads: lane i lands at base + 4 i).  The
+    // window float f = t * NT + tid (4-byte direct loads: lane i lands at
+    // base + 4 i).  Filter slot t covers filter floats FW * (t * NT + tid)
+    // onwards: FW = 4 (16-byte loads) when C_out is even, since then every
+    // channel's chunk of CO_WG x d_filter filters is 16-byte aligned and its
+    // valid part a whole number of 16-byte pieces; FW = 1 otherwise.  The
     // slots keep 32-bit byte offsets from the stage's uniform base pointers.
     const int span2 = a.span2;
     const int wch = CO_WG * df * NB;  // floats per channel of filters
@@ -113,15 +116,24 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
         const int bb = v / D;
         xoffb[t] = 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
     }
+    // filter floats of a channel chunk that belong to channels < C_out
+    const int wvalid = min(CO_WG, a.C_out - co0) * df * NB;
+    constexpr uint32_t NOLOAD = 0xffffffffu;
 #pragma unroll
     for (int t = 0; t < SW; ++t) {
-        const int e = t * NT + tid;
+        const int e = (t * NT + tid) * FW;
         const int c_l = e / wch;
         const int e2 = e - c_l * wch;
-        const int co_l = e2 / (df * NB);
-        const int r = e2 - co_l * (df * NB);
-        const int co = min(co0 + co_l, a.C_out - 1);  // past C_out: unused
-        woffb[t] = 4u * (uint32_t)(c_l * a.C_out * df * NB + (co - co0) * df * NB + r);
+        if constexpr (FW == 4) {
+            // rows past C_out are not loaded: their stale LDS values only
+            // reach accumulator rows of channels that are never stored
+            woffb[t] = e2 < wvalid ? 4u * (uint32_t)(c_l * a.C_out * df * NB + e2) : NOLOAD;
+        } else {
+            const int co_l = e2 / (df * NB);
+            const int r = e2 - co_l * (df * NB);
+            const int co = min(co0 + co_l, a.C_out - 1);  // past C_out: unused
+            woffb[t] = 4u * (uint32_t)(c_l * a.C_out * df * NB + (co - co0) * df * NB + r);
+        }
     }
     const char* xbase = reinterpret_cast<const char*>(a.x + (int64_t)b0 * a.C_in * D * NB);
     const char* wbase = reinterpret_cast<const char*>(a.w + (int64_t)co0 * df * NB);
@@ -133,7 +145,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
         const char* xs = xbase + (int64_t)ci0 * D * NB * 4;
         const char* ws = wbase + (int64_t)ci0 * a.C_out * df * NB * 4;
         float* lx = smem + buf * a.stage_floats + wave_u * 64;
-        float* lw = lx + w_lds;
+        float* lw = smem + buf * a.stage_floats + w_lds + wave_u * 64 * FW;
 #pragma unroll
         for (int t = 0; t < SIN; ++t) {
             if (t * NT + tid < nv * span2)
@@ -142,9 +154,17 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
         }
 #pragma unroll
         for (int t = 0; t < SW; ++t) {
-            if (t * NT + tid < nv * wch)
-                __builtin_amdgcn_global_load_lds(
-                    ws + woffb[t], (__attribute__((address_space(3))) void*)(lw + t * NT), 4, 0, 0);
+            if ((t * NT + tid) * FW < nv * wch && (FW == 1 || woffb[t] != NOLOAD)) {
+                auto* dst = (__attribute__((address_space(3))) void*)(lw + t * NT * FW);
+                // a float source pointer and literal sizes: with a char
+                // pointer the host pass silently drops the 16-byte form's
+                // kernel stub (undefined symbol at load time)
+                const float* src = reinterpret_cast<const float*>(ws + woffb[t]);
+                if constexpr (FW == 4)
+                    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+                else
+                    __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
+            }
         }
     };
 
@@ -311,7 +331,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
     }
 }
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW>
 cliff_status run1d(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NB = 2;
@@ -334,7 +354,7 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     int64_t ccp = 2 * std::max<int64_t>(1, (512 + mfma_per_pair - 1) / mfma_per_pair);
     ccp = std::min<int64_t>(ccp, (lds_budget / (2 * ch_floats * 4)) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, ((int64_t)SIN * NT / (span_max * NB)) & ~int64_t(1));
-    ccp = std::min<int64_t>(ccp, ((int64_t)SW * NT / (CO_WG * df * NB)) & ~int64_t(1));
+    ccp = std::min<int64_t>(ccp, ((int64_t)SW * NT * FW / (CO_WG * df * NB)) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, (p.C_in + 1) & ~int64_t(1));
     if (ccp < 2 || M >= (1ll << 31) || n_blk >= (1ll << 31) ||
         rows_max * p.C_in * D * NB >= (1ll << 30) || ccp * p.C_out * df * NB >= (1ll << 30))
@@ -367,12 +387,20 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
         fprintf(stderr,
                 "cliffconv: conv1d_mfma d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
                 "(%d channels x %d positions), %lld workgroups, %d channels/stage, "
-                "%lld LDS bytes\n",
+                "%lld LDS bytes, %d-byte filter loads\n",
                 (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
-                (long long)lds_bytes);
-    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES>),
+                (long long)lds_bytes, 4 * FW);
+    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
+}
+
+// 16-byte filter loads (fewer slots) when C_out is even, else 4-byte loads.
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW1, int SW4, int WAVES>
+cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
+{
+    if (p.C_out % 2 == 0) return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4>(p, stream);
+    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, WAVES, 1>(p, stream);
 }
 
 // Tile shapes (waves along channels x waves along positions, MFMA tiles per
@@ -384,11 +412,12 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
 template <int DF>
 cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
 {
-    // <DF, WCO, WPOS, MW, NW, input slots, filter slots, waves per SIMD>
-    auto wide = [&] { return run1d<DF, CLIFF_W1>(p, stream); };
-    auto medium = [&] { return run1d<DF, 2, 1, 4, 2, 8, 18, 2>(p, stream); };
-    auto narrow = [&] { return run1d<DF, 1, 4, 1, 4, 16, 4, 2>(p, stream); };
-    auto tiny = [&] { return run1d<DF, 1, 1, 1, 2, 12, 12, 4>(p, stream); };
+    // <DF, WCO, WPOS, MW, NW, input slots, filter slots with 4-byte and with
+    // 16-byte loads, waves per SIMD>
+    auto wide = [&] { return run1d_fw<DF, CLIFF_W1, 18, 6, 2>(p, stream); };
+    auto medium = [&] { return run1d_fw<DF, 2, 1, 4, 2, 8, 18, 9, 2>(p, stream); };
+    auto narrow = [&] { return run1d_fw<DF, 1, 4, 1, 4, 16, 4, 2, 2>(p, stream); };
+    auto tiny = [&] { return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4>(p, stream); };
     switch (p.mfma_shape) {
     case 0: return wide();
     case 1: return medium();

@@ -171,9 +171,10 @@ def test_standalone_act_shape_and_pointer_errors(no_gpu):
 
 
 def test_forced_tile_refuses_unstageable_k1(no_gpu):
-    # the 1-D medium tile (64 channels) cannot stage 64 x 17 filter taps per
-    # channel pair: refused before any launch
-    st = P.clifford_conv_nd_algo(1, (-1,), 2, 3, 64, 60, 17, FAKE, FAKE + (1 << 24),
+    # the 1-D medium tile (64 channels) with 4-byte filter loads (odd C_out)
+    # cannot stage 64 x 17 filter taps per channel pair: refused before any
+    # launch
+    st = P.clifford_conv_nd_algo(1, (-1,), 2, 3, 65, 60, 17, FAKE, FAKE + (1 << 24),
                                  FAKE + (2 << 24), FAKE + (3 << 24), None, 0,
                                  P.ALGO_MFMA_MEDIUM)
     assert st == P.CLIFF_EUNSUPPORTED

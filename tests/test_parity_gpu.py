@@ -51,6 +51,7 @@ SHAPES1 = [
     (2, 5, 3, 17, 3),     # odd channels, C_out < tile
     (3, 4, 20, 60, 17),   # the paper's 1-D signal and filter lengths
     (4, 3, 65, 60, 17),   # two channel blocks of the wide tile
+    (3, 5, 66, 60, 17),   # even C_out: 16-byte filter loads, 2-channel last block
     (5, 7, 9, 10, 1),     # pointwise
     (2, 70, 70, 300, 3),  # several stages, partial last stage, long signal
     (9, 3, 5, 4, 4),      # d_out = 1: each tile spans many batch entries
