@@ -253,46 +253,56 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
 
     const int wtile = CPT * taps2 * NB;  // LDS floats between channel tiles
     auto compute = [&](int buf, int nv) {
-      for (int c_l = 0; c_l < (CCT > 0 ? CCT : nv); ++c_l) {
-        // B fragments index S from the channel's slab, A fragments from the
-        // channel's filters (wofs already includes the filter offset)
-        const float* S = smem + buf * a.stage_floats + c_l * slab_f4 * 4;
-        const float* Sw = smem + buf * a.stage_floats + c_l * wch_f4 * 4;
-        if constexpr (DF > 0) {
-            // Software-pipelined: the raw fragments of step u + 1 (tap, blade
-            // group) are read from LDS while step u's MFMAs issue, one read
-            // after every CLIFF_SGB_IL MFMAs (scheduling-group barriers), so
-            // the matrix pipe never waits behind a clump of reads and no read
-            // sits next to its consumer (measured +1.3-1.9 % for reads issued
-            // ahead of the MFMAs, a further +1-2 % for spreading them).
-            constexpr int T = DF * DF * NH;
-            float fa[2][MW], fb[2][NW];
-            auto ld = [&](int u, float(&A)[MW], float(&Bv)[NW]) {
-                const int h = u % NH, tap = u / NH, qy = tap / DF, qx = tap % DF;
+      if constexpr (DF > 0) {
+        // Software-pipelined over the whole stage: the raw fragments of the
+        // next step (tap, blade group; after a channel's last step, the next
+        // channel's first) are read from LDS while this step's MFMAs issue,
+        // one read after every CLIFF_SGB_IL MFMAs (scheduling-group
+        // barriers), so the matrix pipe never waits behind a clump of reads
+        // and no read sits next to its consumer (measured +1.3-1.9 % for
+        // reads issued ahead of the MFMAs, a further +1-2 % for spreading
+        // them).  With d_filter = 1 (a step or two per channel) the pipeline
+        // also crosses channels, which then go in pairs so that the fragment
+        // buffer of every step is known at compile time; with 3x3(x3) filters
+        // it restarts per channel (crossing measured no faster there, and it
+        // costs registers).
+        constexpr int T = DF * DF * NH;
+        constexpr bool XCH = DF == 1;
+        const int ncl = CCT > 0 ? CCT : nv;
+        const float* S0 = smem + buf * a.stage_floats;
+        float fa[2][MW], fb[2][NW];
+        auto ld = [&](int c, int u, float(&A)[MW], float(&Bv)[NW]) {
+            const float* S = S0 + c * slab_f4 * 4;
+            const float* Sw = S0 + c * wch_f4 * 4;
+            const int h = u % NH, tap = u / NH, qy = tap / DF, qx = tap % DF;
 #pragma unroll
-                for (int mw = 0; mw < MW; ++mw)
-                    A[mw] = Sw[wofs[h] + mw * wtile + tap * NB];
+            for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[wofs[h] + mw * wtile + tap * NB];
 #pragma unroll
-                for (int nw = 0; nw < NW; ++nw)
-                    Bv[nw] = S[xoff[nw] + qy * row_floats + h * D * 4 + qx * 4];
-            };
-            ld(0, fa[0], fb[0]);
+            for (int nw = 0; nw < NW; ++nw)
+                Bv[nw] = S[xoff[nw] + qy * row_floats + h * D * 4 + qx * 4];
+        };
+        auto chan = [&](int c, auto base_c) {
+            constexpr int BASE = decltype(base_c)::value;  // buffer of step 0
 #pragma unroll
             for (int u = 0; u < T; ++u) {
-                if (u + 1 < T) ld(u + 1, fa[(u + 1) & 1], fb[(u + 1) & 1]);
+                const int cur = (BASE + u) & 1;
+                if (u + 1 < T)
+                    ld(c, u + 1, fa[cur ^ 1], fb[cur ^ 1]);
+                else if (XCH && c + 1 < ncl)
+                    ld(c + 1, 0, fa[cur ^ 1], fb[cur ^ 1]);
 #if !CLIFF_SGB_IL
                 // keep the next step's reads ahead of this step's MFMAs
                 __builtin_amdgcn_sched_barrier(0);
 #endif
                 float as[MW];
 #pragma unroll
-                for (int mw = 0; mw < MW; ++mw) as[mw] = fa[u & 1][mw] * sg[u % NH];
+                for (int mw = 0; mw < MW; ++mw) as[mw] = fa[cur][mw] * sg[u % NH];
 #pragma unroll
                 for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
                     for (int nw = 0; nw < NW; ++nw)
                         acc[mw][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            as[mw], fb[u & 1][nw], acc[mw][nw], 0, 0, 0);
+                            as[mw], fb[cur][nw], acc[mw][nw], 0, 0, 0);
 #if CLIFF_SGB_IL
                 // the sign multiplies first, then the next step's LDS reads
                 // spread between this step's MFMAs
@@ -306,8 +316,27 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
 #endif
                 __builtin_amdgcn_sched_barrier(0);
             }
-            continue;
+        };
+        ld(0, 0, fa[0], fb[0]);
+        if constexpr (CCT == 1) {
+            chan(0, std::integral_constant<int, 0>{});
+        } else if constexpr (XCH) {
+            for (int c = 0; c < ncl; c += 2) {
+                chan(c, std::integral_constant<int, 0>{});
+                if (c + 1 < ncl) chan(c + 1, std::integral_constant<int, T & 1>{});
+            }
+        } else {
+            for (int c = 0; c < ncl; ++c) {
+                if (c > 0) ld(c, 0, fa[0], fb[0]);
+                chan(c, std::integral_constant<int, 0>{});
+            }
         }
+      } else {
+      for (int c_l = 0; c_l < (CCT > 0 ? CCT : nv); ++c_l) {
+        // B fragments index S from the channel's slab, A fragments from the
+        // channel's filters (wofs already includes the filter offset)
+        const float* S = smem + buf * a.stage_floats + c_l * slab_f4 * 4;
+        const float* Sw = smem + buf * a.stage_floats + c_l * wch_f4 * 4;
 #pragma unroll
         for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
             for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
@@ -338,6 +367,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                 }
             }
         }
+      }
       }
     };
 
@@ -591,12 +621,16 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
 
 cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream)
 {
+    // 3x3(x3) filters and the linear layer (d_filter = 1) get unrolled,
+    // software-pipelined loops; other sizes a runtime tap loop
     if (p.k == 2) {
         if (p.d_filter == 3) return run_shape<2, 4, 3>(p, stream);
+        if (p.d_filter == 1) return run_shape<2, 4, 1>(p, stream);
         return run_shape<2, 4, 0>(p, stream);
     }
     if (p.k == 3) {
         if (p.d_filter == 3) return run_shape<3, 8, 3>(p, stream);
+        if (p.d_filter == 1) return run_shape<3, 8, 1>(p, stream);
         return run_shape<3, 8, 0>(p, stream);
     }
     return CLIFF_EUNSUPPORTED;
