@@ -63,7 +63,7 @@ def _traffic(workload: str):
 class Runner:
     """Device-resident inputs and preallocated outputs of one workload."""
 
-    def __init__(self, w: W.Workload, fuse_act: bool = True):
+    def __init__(self, w: W.Workload, fuse_act: bool = True, block_path: int = 0):
         import torch
         import paper_2507_01040_amd as P
         self.P, self.torch, self.w = P, torch, w
@@ -83,8 +83,19 @@ class Runner:
         self.outs = [torch.empty(s.output_shape(), dtype=torch.float32, device=dev)
                      for s in w.layers]
         self.g = w.layers[0].g
+        self.block_path = block_path  # for entry "block2": cliff_block_path
 
     def step(self, events=None):
+        if self.w.entry == "block2":
+            # one call of the two-layer block entry point; the first output
+            # buffer is its workspace
+            if events is not None:
+                events[0][0].record()
+            y = self.P.block2(self.x, self.layers[0], self.layers[1], self.g,
+                              out=self.outs[1], workspace=self.outs[0], path=self.block_path)
+            if events is not None:
+                events[0][1].record()
+            return y
         y = self.x
         for li, (f, b, a) in enumerate(self.layers):
             if events is not None:
@@ -121,7 +132,7 @@ class Runner:
         for _ in range(warmup):
             self.step()
         torch.cuda.synchronize()
-        n_l = len(self.layers)
+        n_l = 1 if self.w.entry == "block2" else len(self.layers)
         ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(n_l)] for _ in range(steps)]
         torch.cuda.synchronize()
@@ -162,22 +173,38 @@ def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
                       % (w.name, nb_done - 1, w.layers[0].B, done_flops / 1e9, t_total)}
 
 
+def _flops(x) -> int:
+    """Useful FLOPs of a layer (ConvShape) or of a whole workload."""
+    return x.useful_flops if isinstance(x, W.Workload) else x.useful_flops()
+
+
 def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False):
     w = W.WORKLOADS[name]
     r = Runner(w)
     ms, per_layer = r.time(steps, warmup)
     flops = w.useful_flops
+    timed = [w] if w.entry == "block2" else w.layers  # what each event pair covers
     res = {"workload": name, "ms_per_step": round(ms, 4),
            "useful_gflops": round(flops / (ms * 1e-3) / 1e9, 1),
            "kernel_ms": [round(v, 4) for v in per_layer],
            "kernel_ms_median_min_max": [[round(float(np.median(v)), 4), round(min(v), 4),
                                          round(max(v), 4)] for v in r.last_samples],
            "kernel_algorithmic_GB_s": [round(l.algorithmic_bytes() / (t * 1e-3) / 1e9, 1)
-                                       for l, t in zip(w.layers, per_layer)],
-           "kernel_tflops": [round(l.useful_flops() / (t * 1e-3) / 1e12, 2)
-                             for l, t in zip(w.layers, per_layer)]}
+                                       for l, t in zip(w.layers, per_layer)]
+           if w.entry != "block2" else None,
+           "kernel_tflops": [round(_flops(l) / (t * 1e-3) / 1e12, 2)
+                             for l, t in zip(timed, per_layer)]}
     res["frac_of_fp32_mfma_peak"] = round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
     res["graph_ms_per_step"] = round(r.time_graph(max(steps, 20), warmup), 4)
+    if w.entry == "block2":
+        # the same block as two clifford_conv_nd launches through the workspace
+        import paper_2507_01040_amd as P
+        two = Runner(w, block_path=P.BLOCK_TWO_LAUNCH)
+        ms_two, per_two = two.time(steps, warmup)
+        res["two_launch_ms_per_step"] = round(ms_two, 4)
+        res["two_launch_kernel_ms"] = [round(v, 4) for v in per_two]
+        res["two_launch_graph_ms_per_step"] = round(two.time_graph(max(steps, 20), warmup), 4)
+        del two
     if epilogue_overhead and any(a is not None for a in w.acts):
         plain = Runner(w, fuse_act=False)
         ms_plain, per_plain = plain.time(steps, warmup)

@@ -164,6 +164,60 @@ cliff_status clifford_linear(int k, const int8_t* g, int64_t B, int64_t C_in,
                              const cliff_act_desc* act, void* stream);
 
 /*
+ * Two-layer Clifford block (the basic block pattern of the paper's
+ * network-block experiments, Table 2): convolution (Algorithm 1) + bias +
+ * optional activation (Algorithm 3), then a second convolution of the
+ * intermediate + bias + optional activation:
+ *
+ *   mid    = act1( conv(input,  filters1) + bias1 )   [B, C_mid, d_mid^k, N_B]
+ *   output = act2( conv(mid,    filters2) + bias2 )   [B, C_out, d_out^k, N_B]
+ *
+ * with d_mid = d_image - d_filter + 1 and d_out = d_mid - d_filter + 1 (both
+ * layers share d_filter, no padding, unit stride).
+ *   k, g               as for clifford_conv_nd (k = 1 runs as two launches)
+ *   filters1, bias1    device [C_in, C_mid, d_filter^k, N_B], [C_mid, N_B] or NULL
+ *   act1               NULL or the first activation (weight [C_mid, K], bias [C_mid])
+ *   filters2, bias2    device [C_mid, C_out, d_filter^k, N_B], [C_out, N_B] or NULL
+ *   act2               NULL or the second activation (weight [C_out, K], bias [C_out])
+ *   workspace          device, caller-owned, B * C_mid * d_mid^k * N_B floats:
+ *                      holds `mid` when the block runs as two launches; its
+ *                      contents are unspecified afterwards
+ *   output             device [B, C_out, d_out^k, N_B]
+ * Small blocks (few channels, little work) run as one fused launch that keeps
+ * `mid` in on-chip memory; others as two clifford_conv_nd launches through the
+ * workspace.  Both give the same results up to fp32 rounding order.
+ * Errors: as clifford_conv_nd (CLIFF_EINVAL also for a NULL workspace or
+ * second filter; CLIFF_ESHAPE unless d_image >= 2 d_filter - 1); the
+ * workspace and the output must not overlap each other or any input
+ * (CLIFF_EOVERLAP).  16-byte alignment for all tensors.
+ */
+cliff_status clifford_block2_nd(int k, const int8_t* g, int64_t B, int64_t C_in,
+                                int64_t C_mid, int64_t C_out, int64_t d_image,
+                                int64_t d_filter, const float* input,
+                                const float* filters1, const float* bias1,
+                                const cliff_act_desc* act1, const float* filters2,
+                                const float* bias2, const cliff_act_desc* act2,
+                                float* workspace, float* output, void* stream);
+
+/* Execution path for clifford_block2_nd_path. */
+typedef enum {
+    CLIFF_BLOCK_AUTO = 0,        /* what clifford_block2_nd does */
+    CLIFF_BLOCK_TWO_LAUNCH = 1,  /* two clifford_conv_nd launches via the workspace */
+    CLIFF_BLOCK_FUSED = 2        /* one fused launch (k = 2, 3); CLIFF_EUNSUPPORTED
+                                    when its on-chip working set does not fit */
+} cliff_block_path;
+
+/* clifford_block2_nd with the execution path forced (tests, benchmarks). */
+cliff_status clifford_block2_nd_path(int k, const int8_t* g, int64_t B, int64_t C_in,
+                                     int64_t C_mid, int64_t C_out, int64_t d_image,
+                                     int64_t d_filter, const float* input,
+                                     const float* filters1, const float* bias1,
+                                     const cliff_act_desc* act1, const float* filters2,
+                                     const float* bias2, const cliff_act_desc* act2,
+                                     float* workspace, float* output, void* stream,
+                                     int path);
+
+/*
  * Standalone multivector activation (paper, Algorithm 3).
  *   nb      N_B in {2, 4, 8}
  *   input   device [B, C, P, N_B]   (P positions per channel; P = 1 gives

@@ -25,10 +25,11 @@ STATUS_NAMES = {0: "CLIFF_OK", 1: "CLIFF_EINVAL", 2: "CLIFF_ESHAPE",
 AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
 ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
 ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
+BLOCK_AUTO, BLOCK_TWO_LAUNCH, BLOCK_FUSED = 0, 1, 2
 
 EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
             "multivector_act", "cliffconv_cayley_table", "cliffconv_status_string",
-            "cliffconv_mfma_peak_probe")
+            "cliffconv_mfma_peak_probe", "clifford_block2_nd", "clifford_block2_nd_path")
 
 
 class CliffActDesc(ctypes.Structure):
@@ -67,10 +68,15 @@ def load(path: str = LIB_PATH):
                                     ctypes.POINTER(CliffActDesc), vp, vp, vp]
     lib.cliffconv_cayley_table.argtypes = [i32, vp, vp, vp]
     lib.cliffconv_mfma_peak_probe.argtypes = [i64, ctypes.c_int32, vp, vp]
+    block_args = [i32, vp, i64, i64, i64, i64, i64, i64, vp, vp, vp,
+                  ctypes.POINTER(CliffActDesc), vp, vp, ctypes.POINTER(CliffActDesc), vp, vp, vp]
+    lib.clifford_block2_nd.argtypes = block_args
+    lib.clifford_block2_nd_path.argtypes = block_args + [i32]
     lib.cliffconv_status_string.argtypes = [i32]
     lib.cliffconv_status_string.restype = ctypes.c_char_p
     for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
-                 "multivector_act", "cliffconv_cayley_table", "cliffconv_mfma_peak_probe"):
+                 "multivector_act", "cliffconv_cayley_table", "cliffconv_mfma_peak_probe",
+                 "clifford_block2_nd", "clifford_block2_nd_path"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -137,6 +143,20 @@ def multivector_act(nb: int, B: int, C: int, P: int, act: CliffActDesc,
     return load().multivector_act(nb, B, C, P, ctypes.byref(act),
                                   input_ptr or None, output_ptr or None,
                                   stream or None)
+
+
+def clifford_block2_nd_path(k: int, g: Sequence[int], B: int, C_in: int, C_mid: int,
+                            C_out: int, d_image: int, d_filter: int, input_ptr: int,
+                            filters1_ptr: int, bias1_ptr: int, act1: Optional[CliffActDesc],
+                            filters2_ptr: int, bias2_ptr: int, act2: Optional[CliffActDesc],
+                            workspace_ptr: int, output_ptr: int, stream: int = 0,
+                            path: int = 0) -> int:
+    return load().clifford_block2_nd_path(
+        k, _g_array(g), B, C_in, C_mid, C_out, d_image, d_filter, input_ptr or None,
+        filters1_ptr or None, bias1_ptr or None,
+        ctypes.byref(act1) if act1 is not None else None, filters2_ptr or None,
+        bias2_ptr or None, ctypes.byref(act2) if act2 is not None else None,
+        workspace_ptr or None, output_ptr or None, stream or None, path)
 
 
 def cliffconv_cayley_table(k: int, g: Sequence[int]):
@@ -245,6 +265,47 @@ def act_nd(x, mode: int, blades: Sequence[int], weight=None, bias=None,
                          _stream_ptr(stream))
     if st != CLIFF_OK:
         raise CliffError(st, "multivector_act")
+    return out
+
+
+def _act_desc(act):
+    if act is None:
+        return None
+    mode, blades, aw, ab = act
+    return make_act_desc(mode, blades, aw.data_ptr() if aw is not None else 0,
+                         ab.data_ptr() if ab is not None else 0)
+
+
+def block2(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream=None,
+           path: int = 0):
+    """Two-layer block through clifford_block2_nd: ``layer1``/``layer2`` are
+    (filters, bias or None, act or None) as in block_forward.  The workspace
+    (B * C_mid * d_mid^k * N_B floats) and the output are allocated with
+    torch unless given."""
+    import torch
+    k = len(g)
+    (f1, b1, a1), (f2, b2, a2) = layer1, layer2
+    for t, n in ((x, "x"), (f1, "filters1"), (f2, "filters2")):
+        _check_dev(t, n)
+    B, C_in, d_image = x.shape[0], x.shape[1], x.shape[2]
+    C_mid, C_out, d_filter = f1.shape[1], f2.shape[1], f1.shape[2]
+    d_mid = d_image - d_filter + 1
+    d_out = d_mid - d_filter + 1
+    nb = 1 << k
+    if workspace is None:
+        workspace = torch.empty((B, C_mid) + (d_mid,) * k + (nb,), dtype=torch.float32,
+                                device=x.device)
+    if out is None:
+        out = torch.empty((B, C_out) + (d_out,) * k + (nb,), dtype=torch.float32,
+                          device=x.device)
+    st = clifford_block2_nd_path(k, g, B, C_in, C_mid, C_out, d_image, d_filter,
+                                 x.data_ptr(), f1.data_ptr(),
+                                 b1.data_ptr() if b1 is not None else 0, _act_desc(a1),
+                                 f2.data_ptr(), b2.data_ptr() if b2 is not None else 0,
+                                 _act_desc(a2), workspace.data_ptr(), out.data_ptr(),
+                                 _stream_ptr(stream), path)
+    if st != CLIFF_OK:
+        raise CliffError(st, "clifford_block2_nd")
     return out
 
 

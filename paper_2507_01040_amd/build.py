@@ -16,6 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcliffconv.so")
 SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip",
+           "block_small.hip",
            "mfma_probe.hip"]
 ARCH = "gfx950"
 

@@ -57,6 +57,20 @@ struct ConvProblem {
     int mfma_shape;  // -1: chosen from the problem; 0..3: wide, medium, narrow, tiny
 };
 
+// Two-layer block (conv + bias + act, twice) for the fused small-block kernel.
+struct BlockProblem {
+    int k;
+    int64_t B, C_in, C_mid, C_out, d_image, d_filter;
+    const float* x;
+    const float* w1;
+    const float* b1;
+    const float* w2;
+    const float* b2;
+    float* y;
+    SignMasks sign;
+    ActParams act1, act2;
+};
+
 // Launch logging: with the environment variable CLIFFCONV_DEBUG set to a
 // non-zero value, every launch prints its kernel, grid and tiling to stderr.
 bool debug_enabled();
@@ -67,6 +81,11 @@ cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
 cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream);
 // k = 1 on the matrix cores; CLIFF_EUNSUPPORTED without launching likewise.
 cliff_status launch_conv1d_mfma(const ConvProblem& p, hipStream_t stream);
+// The fused small-block kernel; CLIFF_EUNSUPPORTED without launching when its
+// LDS working set does not fit.
+cliff_status launch_block_small(const BlockProblem& p, hipStream_t stream);
+int64_t block_small_lds_bytes(int k, int64_t C0, int64_t C1, int64_t C2, int64_t d_image,
+                              int64_t d_filter, int64_t R);
 cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P,
                         const ActParams& a, const float* x, float* y,
                         hipStream_t stream);

@@ -188,6 +188,40 @@ def test_mfma_probe_argument_errors(no_gpu):
     assert lib.cliffconv_mfma_peak_probe(1 << 31, 8, FAKE, None) == P.CLIFF_ESHAPE
 
 
+def _block(**kw):
+    args = dict(k=2, g=(1, 1), B=2, C_in=3, C_mid=4, C_out=5, d_image=9, d_filter=3,
+                input_ptr=FAKE, filters1_ptr=FAKE + (1 << 24), bias1_ptr=FAKE + (2 << 24),
+                act1=None, filters2_ptr=FAKE + (3 << 24), bias2_ptr=FAKE + (4 << 24),
+                act2=None, workspace_ptr=FAKE + (5 << 24), output_ptr=FAKE + (6 << 24),
+                stream=0, path=P.BLOCK_AUTO)
+    args.update(kw)
+    return P.clifford_block2_nd_path(**args)
+
+
+BLOCK_ERRORS = [
+    (dict(workspace_ptr=0), P.CLIFF_EINVAL),
+    (dict(filters2_ptr=0), P.CLIFF_EINVAL),
+    (dict(path=3), P.CLIFF_EINVAL),
+    (dict(g=(0, 0)), P.CLIFF_EINVAL),
+    (dict(C_mid=0), P.CLIFF_ESHAPE),
+    (dict(d_image=4), P.CLIFF_ESHAPE),          # d_out would be 0
+    (dict(workspace_ptr=FAKE + (5 << 24) + 4), P.CLIFF_EALIGN),
+    (dict(bias2_ptr=FAKE + (4 << 24) + 8), P.CLIFF_EALIGN),
+    (dict(workspace_ptr=FAKE + (6 << 24) + 64), P.CLIFF_EOVERLAP),   # workspace over output
+    (dict(workspace_ptr=FAKE + (3 << 24) + 16), P.CLIFF_EOVERLAP),   # workspace over filters2
+    (dict(output_ptr=FAKE + 32), P.CLIFF_EOVERLAP),                  # output over input
+]
+
+
+@pytest.mark.parametrize("kw,expect", BLOCK_ERRORS, ids=lambda v: str(v))
+def test_block_argument_errors(no_gpu, kw, expect):
+    assert _block(**kw) == expect
+
+
+def test_block_zero_batch_is_noop(no_gpu):
+    assert _block(B=0) == P.CLIFF_OK
+
+
 def test_bad_algo(no_gpu):
     st = P.clifford_conv_nd_algo(2, (1, 1), 2, 3, 4, 8, 3, FAKE, FAKE + (1 << 24),
                                  FAKE + (2 << 24), FAKE + (3 << 24), None, 0, 7)

@@ -3,7 +3,8 @@ the launch configuration the benchmark times (clifford_conv_nd, automatic
 kernel choice, activation fused into the convolution for the blocks).
 
 The oracle cannot afford every output at these sizes, so it checks:
-  * the 2D tiny workload in full;
+  * the 2D tiny workload and the small block (through the block entry point,
+    fused into one launch) in full;
   * single convolutions: sampled outputs computed one by one by the oracle
     (every batch entry, first and last channels, all four/eight borders of the
     output grid, plus seeded random positions);
@@ -69,6 +70,22 @@ def test_c1_full():
     y = _gpu_block(w, x, ps)
     ref = oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g)
     assert_parity(y, ref)
+
+
+def test_small_block_full():
+    # the small-block workload through the block entry point (one fused
+    # launch), every output against the oracle's fp64 block
+    w = W.WORKLOADS["block2d_c4_d18"]
+    x, ps = W.make_inputs(w)
+    layers = []
+    for p, act in zip(ps, w.acts):
+        layers.append((dev(p.filters), dev(p.bias),
+                       (act.mode, act.blades, dev(p.act_weight), dev(p.act_bias))))
+    y = P.block2(dev(x), layers[0], layers[1], w.layers[0].g)
+    torch.cuda.synchronize()
+    ref = oracle.block(x, [(p.filters, p.bias, (a.mode, a.blades, p.act_weight, p.act_bias))
+                           for p, a in zip(ps, w.acts)], w.layers[0].g)
+    assert_parity(y.cpu().numpy(), ref)
 
 
 @pytest.mark.parametrize("name", ["conv2d_c64_d128", "conv3d_c32_d32", "conv1d_c64_d60"])

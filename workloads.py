@@ -93,6 +93,9 @@ class Workload:
     filter_bound: Tuple[float, ...]  # U(-a, a) half-width per layer
     bias_std: float
     act_bias_std: float = 0.1
+    # "layers": one clifford_conv_nd launch per layer; "block2": the two-layer
+    # block entry point (fused into one launch when small)
+    entry: str = "layers"
 
     @property
     def useful_flops(self) -> int:
@@ -136,6 +139,13 @@ WORKLOADS = {
         _conv_layers(3, (1, 1, 1), 8, 64, 36, 3, 2),
         (ActSpec(AGG_MEAN, tuple(range(8))), ActSpec(AGG_MEAN, tuple(range(8)))),
         (_fan_bound(64, 3, 3),) * 2, bias_std=0.1),
+    # a block in the paper's small-parameter regime (C = 4, as the 2D tiny
+    # workload): latency-bound, runs as one fused launch
+    "block2d_c4_d18": Workload(
+        "block2d_c4_d18", 1006,
+        _conv_layers(2, (1, 1), 8, 4, 18, 3, 2),
+        (ActSpec(AGG_LINEAR, (0, 1, 2, 3)), ActSpec(AGG_LINEAR, (0, 1, 2, 3))),
+        (_fan_bound(4, 3, 2),) * 2, bias_std=1.0, entry="block2"),
     # the paper's 1-D layer (d_image 60, d_filter 17) at a GPU-sized batch
     "conv1d_c64_d60": Workload(
         "conv1d_c64_d60", 1005,
