@@ -126,8 +126,8 @@ typedef enum {
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32
                                    positions */
     CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 8 / 4 channels x 256 positions */
-    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 8 / 4 / 2 channels x 32 positions,
-                                   one wave */
+    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 8 / 4 / 2 channels x 32 positions
+                                   (k = 2, 3: the K loop split over 4 waves) */
 } cliff_algo;
 
 /*

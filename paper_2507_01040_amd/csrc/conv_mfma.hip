@@ -64,23 +64,19 @@ struct MfmaArgs {
     ActParams act;
 };
 
-// Stage buffers: 3 (two stages in flight) for one-wave 2D workgroups (measured
-// 3-5 % faster on small 2D problems, 1-2 % slower in 3D), else 2.
-constexpr int n_stage_buffers(int waves_per_wg, int kd)
-{
-    return waves_per_wg == 1 && kd == 2 ? 3 : 2;
-}
-
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
-          int WAVES_PER_SIMD>
-__global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_kernel(MfmaArgs a)
+          int WAVES_PER_SIMD, int WK>
+__global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfma_kernel(
+    MfmaArgs a)
 {
-    constexpr int NT = 64 * WCO * WPOS;
+    // WK > 1: WK waves share every output tile, each taking every WK-th input
+    // channel of a stage; their partial sums meet in LDS before the epilogue
+    static_assert(WK == 1 || CCT != 1, "a K split needs several channels per stage");
+    constexpr int NT = 64 * WCO * WPOS * WK;
     constexpr int CPT = 16 / NB;  // output channels per 16-row tile
     constexpr int CO_WG = WCO * MW * CPT;
     constexpr int P = WPOS * NW * 16;
     constexpr int NH = NB / 4;  // groups of 4 input blades (MFMA K = 4)
-    constexpr int NBUF = n_stage_buffers(WCO * WPOS, KD);
 
     extern __shared__ f4 smem4[];
     float* smem = reinterpret_cast<float*>(smem4);
@@ -209,19 +205,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                                        : (goff[t] >= 0 ? f < nv * slab_f4
                                                        : (f < total_f4 &&
                                                           f - cc * slab_f4 < nv * wch_f4));
-            if constexpr (NBUF == 2) {
-                if (load) {
-                    const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
-                    __builtin_amdgcn_global_load_lds(
-                        src, (__attribute__((address_space(3))) void*)(lbase + t * NT * 4), 16,
-                        0, 0);
-                }
-            } else {
-                // every slot loads (an unused one re-reads the stage's first
-                // float4 into its own, unread, place of the padded buffer), so
-                // each stage is exactly SLOTS loads per wave and the main loop
-                // can wait for one stage while the next is still in flight
-                const float* src = !load ? xs : goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
+            if (load) {
+                const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
                 __builtin_amdgcn_global_load_lds(
                     src, (__attribute__((address_space(3))) void*)(lbase + t * NT * 4), 16, 0,
                     0);
@@ -232,8 +217,10 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
     // Per-lane constants of the MFMA fragments.
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wco = wave % WCO;
-    const int wpos = wave / WCO;
+    const int wk = wave / (WCO * WPOS);     // K slice of this wave
+    const int wrest = wave - wk * (WCO * WPOS);
+    const int wco = wrest % WCO;
+    const int wpos = wrest / WCO;
     const int mrow = lane & 15;
     const int kk = lane >> 4;
 
@@ -287,7 +274,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
         // costs registers).
         constexpr int T = DF * DF * NH;
         constexpr bool XCH = DF == 1;
-        // Prefetch distance in steps: the one-wave tile has only 2 MFMAs (64
+        // Prefetch distance in steps: the tiny tile has only 2 MFMAs (64
         // cycles) per step, less than the LDS latency, so it reads 3 steps
         // ahead; the others 1.
         constexpr int PF = !XCH && MW * NW <= 2 ? 3 : 1;
@@ -313,8 +300,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
                 const int nxt = (BASE + u + PF) % RB;
                 if (u + PF < T)
                     ld(c, u + PF, fa[nxt], fb[nxt]);
-                else if (XCH && c + 1 < ncl)
-                    ld(c + 1, 0, fa[nxt], fb[nxt]);
+                else if (XCH && c + WK < ncl)
+                    ld(c + WK, 0, fa[nxt], fb[nxt]);
 #if !CLIFF_SGB_IL
                 // keep the next step's reads ahead of this step's MFMAs
                 __builtin_amdgcn_sched_barrier(0);
@@ -347,22 +334,24 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
             for (int u = 0; u < PF; ++u)
                 if (u < T) ld(c, u, fa[u], fb[u]);
         };
-        prologue(0);
         if constexpr (CCT == 1) {
+            prologue(0);
             chan(0, std::integral_constant<int, 0>{});
         } else if constexpr (XCH) {
-            for (int c = 0; c < ncl; c += 2) {
+            // this wave's channels wk, wk + WK, ...
+            if (wk < ncl) prologue(wk);
+            for (int c = wk; c < ncl; c += 2 * WK) {
                 chan(c, std::integral_constant<int, 0>{});
-                if (c + 1 < ncl) chan(c + 1, std::integral_constant<int, T & 1>{});
+                if (c + WK < ncl) chan(c + WK, std::integral_constant<int, T & 1>{});
             }
         } else {
-            for (int c = 0; c < ncl; ++c) {
-                if (c > 0) prologue(c);
+            for (int c = wk; c < ncl; c += WK) {
+                prologue(c);
                 chan(c, std::integral_constant<int, 0>{});
             }
         }
       } else {
-      for (int c_l = 0; c_l < (CCT > 0 ? CCT : nv); ++c_l) {
+      for (int c_l = wk; c_l < (CCT > 0 ? CCT : nv); c_l += WK) {
         // B fragments index S from the channel's slab, A fragments from the
         // channel's filters (wofs already includes the filter offset)
         const float* S = smem + buf * a.stage_floats + c_l * slab_f4 * 4;
@@ -401,42 +390,41 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES_PER_SIMD) void conv_mfma_ker
       }
     };
 
-    // Main loop: one barrier per stage.
-    if constexpr (NBUF == 2) {
-        // the next stage's global loads are in flight while the current one
-        // is multiplied
-        load_stage(0, 0);
+    // Main loop: one barrier per stage; the next stage's global loads are in
+    // flight while the current one is multiplied.
+    load_stage(0, 0);
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int s = 0; s < a.n_stage; ++s) {
+        // buffer (s+1)&1 was last read in iteration s-1, before the barrier
+        if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
+        int ci0, qz;
+        compute(s & 1, stage_channels(s, ci0, qz));
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        for (int s = 0; s < a.n_stage; ++s) {
-            // buffer (s+1)&1 was last read in iteration s-1, before the barrier
-            if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
-            int ci0, qz;
-            compute(s & 1, stage_channels(s, ci0, qz));
-            __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
+    }
+
+    if constexpr (WK > 1) {
+        // The stage loop ended with a barrier, so LDS is free: K slices
+        // 1..WK-1 leave their partial sums there, slice 0 adds them and stores.
+        constexpr int PER = WCO * WPOS * MW * NW;  // f4 per lane per slice
+        if (wk > 0) {
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw)
+                    smem4[((wk - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane] =
+                        acc[mw][nw];
         }
-    } else {
-        // two stages in flight: a one-wave workgroup's stage is too short to
-        // cover the HBM latency of the next one.  Each stage is SLOTS loads
-        // per wave, so waiting for stage s while s + 1 is outstanding is
-        // vmcnt(SLOTS).
-        load_stage(0, 0);
-        if (a.n_stage > 1) load_stage(1, 1);
-        for (int s = 0; s < a.n_stage; ++s) {
-            if (s + 1 < a.n_stage)
-                __asm__ volatile("s_waitcnt vmcnt(%0)" ::"i"(SLOTS) : "memory");
-            else
-                __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            // every wave has its stage-s loads and has finished stage s - 1,
-            // whose buffer (s + 2) % 3 is reloaded next.  A plain s_barrier:
-            // __syncthreads() would also wait for stage s + 1's loads.  A
-            // one-wave workgroup needs none.
-            if constexpr (NT > 64) __builtin_amdgcn_s_barrier();
-            if (s + 2 < a.n_stage) load_stage(s + 2, (s + 2) % 3);
-            int ci0, qz;
-            compute(s % 3, stage_channels(s, ci0, qz));
-        }
+        __syncthreads();
+        if (wk > 0) return;  // wave-uniform: no barrier follows
+#pragma unroll
+        for (int k = 1; k < WK; ++k)
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw)
+                    acc[mw][nw] += smem4[((k - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane];
     }
 
     // Epilogue: bias, optional multivector activation, 16-byte stores.
@@ -486,10 +474,10 @@ struct TileCfg {
 };
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
-          int WAVES>
+          int WAVES, int WK>
 cliff_status run(const ConvProblem& p, hipStream_t stream)
 {
-    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int NT = 64 * WCO * WPOS * WK;
     constexpr int CPT = 16 / NB;
     constexpr int CO_WG = WCO * MW * CPT;
     constexpr int P = WPOS * NW * 16;
@@ -512,17 +500,17 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     // LDS budget (two buffers) and the staging slots.
     constexpr int64_t LDS_BUDGET = 64 * 1024;
     constexpr int64_t MFMA_PER_STAGE = 512;
-    constexpr int NBUF = n_stage_buffers(WCO * WPOS, KD);
     const int64_t mfma_per_ch = df * df * (NB / 4) * MW * NW;
     int64_t cc = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
-    cc = std::min<int64_t>(cc, LDS_BUDGET / (NBUF * ch_floats * 4));
+    cc = std::min<int64_t>(cc, LDS_BUDGET / (2 * ch_floats * 4));
     cc = std::min<int64_t>(cc, (int64_t)SLOTS * NT / (ch_floats / 4));
     if (CCT > 0) cc = cc >= CCT ? CCT : 0;
+    if (WK > 1 && cc > WK) cc -= cc % WK;  // equal channel shares for the K slices
     if (cc < 1) return CLIFF_EUNSUPPORTED;
-    // with 3 buffers every slot loads, so a buffer spans all SLOTS x NT float4
-    const int64_t stage_floats =
-        NBUF == 3 ? std::max<int64_t>(cc * ch_floats, (int64_t)SLOTS * NT * 4) : cc * ch_floats;
-    const int64_t lds_bytes = NBUF * stage_floats * 4;
+    const int64_t stage_floats = cc * ch_floats;
+    // the K split's partial sums reuse the stage buffers after the loop
+    const int64_t red_bytes = (int64_t)(WK - 1) * WCO * WPOS * MW * NW * 64 * 16;
+    const int64_t lds_bytes = std::max<int64_t>(2 * stage_floats * 4, red_bytes);
     if (lds_bytes > 160 * 1024) return CLIFF_EUNSUPPORTED;
     // staging offsets are 32-bit, relative to the block's first plane
     int64_t img = NB;
@@ -554,10 +542,11 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     if (debug_enabled())
         fprintf(stderr,
                 "cliffconv: conv_mfma k=%d d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
-                "(%d channels x %d positions), %lld workgroups, %d channels/stage, %lld LDS bytes\n",
-                KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
+                "(%d channels x %d positions), K split over %d waves, %lld workgroups, "
+                "%d channels/stage, %lld LDS bytes\n",
+                KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, WK, (long long)n_blk, (int)cc,
                 (long long)lds_bytes);
-    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>),
+    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
@@ -570,8 +559,8 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 //          2 waves/SIMD), k = 3 does best with 4 x 4 tiles at 3 waves/SIMD
 //  medium  many channels, few positions: 32 positions per workgroup
 //  narrow  few channels, many positions
-//  tiny    one wave, 4 (k = 2) or 2 (k = 3) channels by 32 positions: small
-//          problems, spread over as many CUs as possible
+//  tiny    4 (k = 2) or 2 (k = 3) channels by 32 positions, the K loop split
+//          over 4 waves: small problems, spread over as many CUs as possible
 #ifndef CLIFF_W2
 #define CLIFF_W2 4, 1, 4, 8, 6, 2  // WCO, WPOS, MW, NW, SLOTS, waves/SIMD (k = 2)
 #endif
@@ -582,10 +571,16 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
 #define CLIFF_NARROW 1, 4, 2, 4, 8, 2
-#define CLIFF_TINY2 1, 1, 1, 2, 12, 4
-#define CLIFF_TINY3 1, 1, 1, 2, 12, 3
+// tiny: one 4 (2D) / 2 (3D) channel x 32 position tile per workgroup, its K
+// loop split over 4 waves (measured 1.1-2.2x faster than one wave on small
+// problems, whose critical path is the K loop, not the tile)
+#ifndef CLIFF_TINY_WK
+#define CLIFF_TINY_WK 4
+#endif
+#define CLIFF_TINY2 1, 1, 1, 2, 12, 4, CLIFF_TINY_WK
+#define CLIFF_TINY3 1, 1, 1, 2, 12, 3, CLIFF_TINY_WK
 
-template <int NB, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
+template <int NB, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES, int WK = 1>
 struct Shape {
     static constexpr int co_wg = WCO * MW * (16 / NB);
     static constexpr int pos = WPOS * NW * 16;
@@ -595,10 +590,12 @@ struct Shape {
     }
 };
 
-template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES>
-cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream, Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES>)
+template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES,
+          int WK>
+cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream,
+                           Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>)
 {
-    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES>(p, stream);
+    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>(p, stream);
 }
 
 template <int KD, int NB, int DF, class Wide>
@@ -628,8 +625,8 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
     // Shape choice, from timing every shape on 2D/3D convolutions and linear
     // layers (d_image = d_filter = 1) of 7 to 9,000 GFLOP on MI355X (256 CUs):
     // wide once it fills every CU; medium for linear layers with >= 128
-    // workgroups; narrow from 128 workgroups; tiny (one wave per workgroup,
-    // the most workgroups) for the smallest problems.  A shape whose LDS or
+    // workgroups; narrow from 128 workgroups; tiny (the smallest tile, the
+    // most workgroups) for the smallest problems.  A shape whose LDS or
     // staging needs do not fit returns CLIFF_EUNSUPPORTED and the next one in
     // the order is tried.
     const bool wide_ok = p.C_out * 2 > Wide::co_wg;
