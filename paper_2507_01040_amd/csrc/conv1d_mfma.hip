@@ -65,11 +65,14 @@ struct C1Args {
     ActParams act;
 };
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW>
-__global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1Args a)
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int WK>
+__global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kernel(C1Args a)
 {
+    // WK > 1: WK waves share every output tile, each taking every WK-th
+    // channel pair of a stage; their partial sums meet in LDS before the
+    // epilogue
     constexpr int NB = 2;
-    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int NT = 64 * WCO * WPOS * WK;
     constexpr int CPT = 8;  // output channels per 16-row tile
     constexpr int CO_WG = WCO * MW * CPT;
     constexpr int P = WPOS * NW * 16;
@@ -173,8 +176,10 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
 
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wco = wave % WCO;
-    const int wpos = wave / WCO;
+    const int wk = wave / (WCO * WPOS);  // K slice of this wave
+    const int wrest = wave - wk * (WCO * WPOS);
+    const int wco = wrest % WCO;
+    const int wpos = wrest / WCO;
     const int mrow = lane & 15;
     const int kk = lane >> 4;
     const int c_sub = kk >> 1;  // channel of the pair
@@ -270,8 +275,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
     auto compute = [&](int buf, int nv) {
         const float* S0 = smem + buf * a.stage_floats;
         const int nfull = nv & ~1;
-        for (int c_l = 0; c_l < nfull; c_l += 2) pair(S0, c_l, std::false_type{});
-        if (nv & 1) pair(S0, nfull, std::true_type{});
+        for (int c_l = 2 * wk; c_l < nfull; c_l += 2 * WK) pair(S0, c_l, std::false_type{});
+        if ((nv & 1) && (nfull / 2) % WK == wk) pair(S0, nfull, std::true_type{});
     };
 
     load_stage(0, 0);
@@ -283,6 +288,29 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
         compute(s & 1, stage_channels(s));
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
+    }
+
+    if constexpr (WK > 1) {
+        // The stage loop ended with a barrier, so LDS is free: K slices
+        // 1..WK-1 leave their partial sums there, slice 0 adds them and stores.
+        constexpr int PER = WCO * WPOS * MW * NW;  // f4 per lane per slice
+        if (wk > 0) {
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw)
+                    smem4[((wk - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane] =
+                        acc[mw][nw];
+        }
+        __syncthreads();
+        if (wk > 0) return;  // wave-uniform: no barrier follows
+#pragma unroll
+        for (int k = 1; k < WK; ++k)
+#pragma unroll
+            for (int mw = 0; mw < MW; ++mw)
+#pragma unroll
+                for (int nw = 0; nw < NW; ++nw)
+                    acc[mw][nw] += smem4[((k - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane];
     }
 
     // Epilogue: lane row 4 kk + r is channel 2 kk + r / 2, blade r % 2.
@@ -334,11 +362,11 @@ __global__ __launch_bounds__(64 * WCO * WPOS, WAVES) void conv1d_mfma_kernel(C1A
     }
 }
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int WK>
 cliff_status run1d(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NB = 2;
-    constexpr int NT = 64 * WCO * WPOS;
+    constexpr int NT = 64 * WCO * WPOS * WK;
     constexpr int CO_WG = WCO * MW * 8;
     constexpr int P = WPOS * NW * 16;
     const int64_t D = p.d_image, Do = p.d_out, df = p.d_filter;
@@ -351,7 +379,7 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     const int64_t span_max = P + rows_max * (df - 1);
     const int64_t ch_floats = span_max * NB + CO_WG * df * NB;
     // LDS: two stage buffers per workgroup, WAVES waves per SIMD resident
-    const int64_t wg_per_cu = std::max<int64_t>(1, 4 * WAVES / (WCO * WPOS));
+    const int64_t wg_per_cu = std::max<int64_t>(1, 4 * WAVES / (WCO * WPOS * WK));
     const int64_t lds_budget = std::min<int64_t>(CLIFF_LDS1, 160 * 1024 / wg_per_cu);
     const int64_t mfma_per_pair = df * MW * NW;
     int64_t ccp = 2 * std::max<int64_t>(1, (512 + mfma_per_pair - 1) / mfma_per_pair);
@@ -359,12 +387,15 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     ccp = std::min<int64_t>(ccp, ((int64_t)SIN * NT / (span_max * NB)) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, ((int64_t)SW * NT * FW / (CO_WG * df * NB)) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, (p.C_in + 1) & ~int64_t(1));
+    if (WK > 1 && ccp > 2 * WK) ccp -= ccp % (2 * WK);  // equal pair shares for the K slices
     if (ccp < 2 || M >= (1ll << 31) || n_blk >= (1ll << 31) ||
         rows_max * p.C_in * D * NB >= (1ll << 30) || ccp * p.C_out * df * NB >= (1ll << 30))
         return CLIFF_EUNSUPPORTED;
     const int64_t cc = std::min<int64_t>(ccp, p.C_in);
     const int64_t stage_floats = ccp * ch_floats;
-    const int64_t lds_bytes = 2 * stage_floats * 4;
+    // the K split's partial sums reuse the stage buffers after the loop
+    const int64_t red_bytes = (int64_t)(WK - 1) * WCO * WPOS * MW * NW * 64 * 16;
+    const int64_t lds_bytes = std::max<int64_t>(2 * stage_floats * 4, red_bytes);
 
     C1Args a;
     a.x = p.x;
@@ -393,17 +424,18 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
                 "%lld LDS bytes, %d-byte filter loads\n",
                 (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
                 (long long)lds_bytes, 4 * FW);
-    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW>),
+    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
 
 // 16-byte filter loads (fewer slots) when C_out is even, else 4-byte loads.
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW1, int SW4, int WAVES>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW1, int SW4, int WAVES,
+          int WK = 1>
 cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
 {
-    if (p.C_out % 2 == 0) return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4>(p, stream);
-    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, WAVES, 1>(p, stream);
+    if (p.C_out % 2 == 0) return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4, WK>(p, stream);
+    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, WAVES, 1, WK>(p, stream);
 }
 
 // Tile shapes (waves along channels x waves along positions, MFMA tiles per
@@ -411,7 +443,8 @@ cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
 //   wide   2x2 waves of 4x4 tiles: 64 channels x 128 positions
 //   medium 2x1 waves of 4x2 tiles: 64 channels x  32 positions
 //   narrow 1x4 waves of 1x4 tiles:  8 channels x 256 positions
-//   tiny   one wave of 1x2 tiles:   8 channels x  32 positions
+//   tiny   1x2 tiles:                8 channels x  32 positions (long K loops
+//          split over 4 waves)
 template <int DF>
 cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
 {
@@ -422,7 +455,16 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     };
     auto medium = [&] { return run1d_fw<DF, 2, 1, 4, 2, 8, 18, 9, 2>(p, stream); };
     auto narrow = [&] { return run1d_fw<DF, 1, 4, 1, 4, 16, 4, 2, 2>(p, stream); };
-    auto tiny = [&] { return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4>(p, stream); };
+    // the tiny tile splits its K loop over 4 waves when that loop is long and
+    // the workgroups are few (measured 1.5-1.8x faster there; with 2816
+    // workgroups, or only 12 K steps, one wave per tile is 7-20 % faster)
+    auto tiny = [&] {
+        const int64_t tiles = ((p.B * p.d_out + 31) / 32) * ((p.C_out + 7) / 8);
+        const int64_t ksteps = (p.C_in + 1) / 2 * p.d_filter;
+        if (tiles < 1024 && ksteps >= 32)
+            return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4, 4>(p, stream);
+        return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4, 1>(p, stream);
+    };
     switch (p.mfma_shape) {
     case 0: return wide();
     case 1: return medium();

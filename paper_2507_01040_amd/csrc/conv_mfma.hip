@@ -30,11 +30,12 @@
 //     [row][half][x][4] for N_B = 8 so that a fragment read is 64 consecutive
 //     words);
 //   * the raw filters [co][tap][blade] of this stage (no expansion).
+// The smallest tile splits its K loop over several waves of the workgroup
+// (WK), whose partial sums meet in LDS before the epilogue.
 #include <stdio.h>
 
 #include <algorithm>
 #include <type_traits>
-
 
 #include "common.hpp"
 #include "epilogue.hpp"

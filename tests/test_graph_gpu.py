@@ -41,3 +41,34 @@ def test_graph_replay_matches_eager(k):
         graph.replay()
         torch.cuda.synchronize()
         assert torch.equal(out_g, eager), "replay %d differs from eager" % rep
+
+
+@pytest.mark.parametrize("path", [P.BLOCK_FUSED, P.BLOCK_TWO_LAUNCH], ids=["fused", "two_launch"])
+def test_graph_replay_block2(path):
+    # the two-layer block entry point, both paths, captured and replayed
+    g = (1, 1)
+    _, x, f1, b1 = W.random_conv_case(510, 2, g, 4, 4, 6, 18, 3)
+    _, _, f2, b2 = W.random_conv_case(511, 2, g, 4, 6, 4, 16, 3)
+    rng = np.random.default_rng(9)
+    aw = dev(rng.standard_normal((6, 4)).astype(np.float32))
+    ab = dev(rng.standard_normal(6).astype(np.float32))
+    l1 = (dev(f1), dev(b1), (P.AGG_LINEAR, (0, 1, 2, 3), aw, ab))
+    l2 = (dev(f2), dev(b2), (P.AGG_MEAN, (1, 2), None, None))
+    xt = dev(x)
+    ws = torch.empty((4, 6, 16, 16, 4), device="cuda:0")
+    out_g = torch.empty((4, 4, 14, 14, 4), device="cuda:0")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        P.block2(xt, l1, l2, g, out=out_g, workspace=ws, path=path)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.block2(xt, l1, l2, g, out=out_g, workspace=ws, path=path)
+    for rep in range(3):
+        xt.copy_(dev(x * (1.0 - 0.3 * rep)))
+        eager = P.block2(xt, l1, l2, g, path=path)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, eager), "replay %d differs from eager" % rep
