@@ -308,8 +308,8 @@ def measure_act(nb: int, B: int, C: int, Pn: int, mode: int, blades, steps: int 
             "device_copy_GB_s": round(nbytes / (ms_copy * 1e-3) / 1e9, 1)}
 
 
-def measure_linear(k: int, B: int, C: int, steps: int = 20, warmup: int = 3):
-    """Clifford linear layer (Algorithm 2) [B, C, N_B] x [C, C, N_B]: mean
+def measure_linear(k: int, B: int, C: int, steps: int = 30, warmup: int = 10):
+    """Clifford linear layer (Algorithm 2) [B, C, N_B] x [C, C, N_B]: median
     kernel time and useful TFLOP/s (2 B C^2 N_B^2 FLOPs)."""
     import torch
     import paper_2507_01040_amd as P
@@ -329,7 +329,7 @@ def measure_linear(k: int, B: int, C: int, steps: int = 20, warmup: int = 3):
         P.linear(x, w, b, g, out=out)
         e1.record()
     torch.cuda.synchronize()
-    ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+    ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
     flops = 2 * B * C * C * nb * nb
     nbytes = 4 * (x.numel() + w.numel() + b.numel() + out.numel())
     return {"k": k, "B": B, "C_in": C, "C_out": C, "kernel_ms": round(ms, 4),
@@ -418,7 +418,8 @@ def main():
             torch.cuda.empty_cache()
         line["workloads"] = extra
         # Clifford linear layers at the paper's C = 32 with GPU-sized batches
-        line["clifford_linear"] = [measure_linear(2, 1 << 20, 32), measure_linear(3, 1 << 19, 32)]
+        line["clifford_linear"] = [measure_linear(2, 1 << 20, 32), measure_linear(3, 1 << 19, 32),
+                                   measure_linear(1, 1 << 21, 32)]
         # standalone activation at the blocks' intermediate shapes (HBM bound)
         line["multivector_act"] = [
             measure_act(4, 8, 64, 128 * 128, W.AGG_LINEAR, (0, 1, 2, 3)),

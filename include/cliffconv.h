@@ -126,8 +126,13 @@ typedef enum {
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32
                                    positions */
     CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 8 / 4 channels x 256 positions */
-    CLIFF_ALGO_MFMA_TINY = 6    /* MFMA, 8 / 4 / 2 channels x 32 positions
+    CLIFF_ALGO_MFMA_TINY = 6,   /* MFMA, 8 / 4 / 2 channels x 32 positions
                                    (k = 2, 3: the K loop split over 4 waves) */
+    CLIFF_ALGO_MFMA_STREAM = 7  /* MFMA, linear layers only (d_image =
+                                   d_filter = 1, C_in = C_out, C_out N_B = 64,
+                                   128 or 256): persistent waves that stream
+                                   16-64 positions at a time past the weight
+                                   held in LDS */
 } cliff_algo;
 
 /*
@@ -156,7 +161,10 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
  *   bias      device [C_out, N_B], or NULL for zero
  *   output    device [B, C_out, N_B]; must not overlap any input
  * Same alignment, size, error and stream rules as clifford_conv_nd; it is
- * the convolution with d_image = d_filter = 1 and runs on the same kernels.
+ * the convolution with d_image = d_filter = 1.  Square layers with
+ * C_out N_B = 64, 128 or 256 and B >= 16384 run on a streamed kernel that
+ * keeps the weight in LDS (CLIFF_ALGO_MFMA_STREAM); other layers on the
+ * convolution kernels.
  */
 cliff_status clifford_linear(int k, const int8_t* g, int64_t B, int64_t C_in,
                              int64_t C_out, const float* input, const float* weight,

@@ -25,6 +25,7 @@ STATUS_NAMES = {0: "CLIFF_OK", 1: "CLIFF_EINVAL", 2: "CLIFF_ESHAPE",
 AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
 ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
 ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
+ALGO_MFMA_STREAM = 7  # linear layers only
 BLOCK_AUTO, BLOCK_TWO_LAUNCH, BLOCK_FUSED = 0, 1, 2
 
 EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",

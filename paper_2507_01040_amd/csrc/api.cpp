@@ -150,6 +150,13 @@ ActParams to_params(const cliff_act_desc* act)
     return a;
 }
 
+// Linear layers: the streamed kernel once it has enough 16-position wave
+// tiles to give every SIMD of the chip several of them.
+bool linear_stream_pays(const ConvProblem& p)
+{
+    return p.B >= 16 * 1024;
+}
+
 }  // namespace
 
 extern "C" {
@@ -162,7 +169,7 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
 {
     if (!g || !input || !filters || !output) return CLIFF_EINVAL;
     if (!valid_k(k) || !valid_signature(k, g)) return CLIFF_EINVAL;
-    if (algo < CLIFF_ALGO_AUTO || algo > CLIFF_ALGO_MFMA_TINY) return CLIFF_EINVAL;
+    if (algo < CLIFF_ALGO_AUTO || algo > CLIFF_ALGO_MFMA_STREAM) return CLIFF_EINVAL;
     const int nb = 1 << k;
     bool linear = false;
     if (act) {
@@ -206,10 +213,18 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B, int64_t C_
     p.y = output;
     p.sign = pack_signs(nb, sign);
     p.act = to_params(act);
-    p.mfma_shape = algo >= CLIFF_ALGO_MFMA_WIDE ? algo - CLIFF_ALGO_MFMA_WIDE : -1;
+    p.mfma_shape = algo >= CLIFF_ALGO_MFMA_WIDE && algo <= CLIFF_ALGO_MFMA_TINY
+                       ? algo - CLIFF_ALGO_MFMA_WIDE
+                       : -1;
     hipStream_t st = (hipStream_t)stream;
 
     if (algo == CLIFF_ALGO_DIRECT) return launch_conv_direct(p, st);
+    if (algo == CLIFF_ALGO_MFMA_STREAM) return launch_linear_mfma(p, st);
+    if ((algo == CLIFF_ALGO_AUTO || algo == CLIFF_ALGO_MFMA) && d_image == 1 &&
+        linear_stream_pays(p)) {
+        const cliff_status s = launch_linear_mfma(p, st);
+        if (s != CLIFF_EUNSUPPORTED) return s;
+    }
     const cliff_status s = k == 1 ? launch_conv1d_mfma(p, st) : launch_conv_mfma(p, st);
     if (s != CLIFF_EUNSUPPORTED || mfma_forced) return s;
     return launch_conv_direct(p, st);

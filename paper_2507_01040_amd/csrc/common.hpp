@@ -81,6 +81,9 @@ cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
 cliff_status launch_conv_mfma(const ConvProblem& p, hipStream_t stream);
 // k = 1 on the matrix cores; CLIFF_EUNSUPPORTED without launching likewise.
 cliff_status launch_conv1d_mfma(const ConvProblem& p, hipStream_t stream);
+// Linear layers (d_image = d_filter = 1) on the streamed MFMA kernel;
+// CLIFF_EUNSUPPORTED without launching when the channel counts do not fit it.
+cliff_status launch_linear_mfma(const ConvProblem& p, hipStream_t stream);
 // The fused small-block kernel; CLIFF_EUNSUPPORTED without launching when its
 // LDS working set does not fit.
 cliff_status launch_block_small(const BlockProblem& p, hipStream_t stream);

@@ -1,0 +1,349 @@
+// Clifford linear layer (paper, Algorithm 2) as a streamed GEMM on the fp32
+// matrix cores (v_mfma_f32_16x16x4_f32).
+//
+// With one position and one tap the layer is Y = X E^T + bias, with X the
+// input as stored ([B, K], K = C_in N_B), Y the output ([B, N], N = C_out N_B)
+// and E the expanded weight, E[(co, i), (ci, j)] = s(i, j) w[ci, co, i ^ j]
+// (table sign and source blade as in the convolution).  B is large and N, K
+// are small (the paper's linear layers have 32 channels), so:
+//  * every workgroup copies the raw weight [C_in, C_out, N_B] into LDS once;
+//    A fragments are read from there and the sign applied in a register, so
+//    the expanded weight exists nowhere;
+//  * each wave owns whole rows of Y (a tile of 16 * NWW positions by all N
+//    columns) and streams its tiles without any barrier: B fragments come from
+//    HBM straight into registers, PF chunks of 16 K values ahead, across tile
+//    boundaries, so one tile's loads and the previous tile's stores overlap
+//    the current tile's MFMAs;
+//  * the grid is persistent (as many workgroups as fit at once), each wave
+//    taking every (number of waves)-th tile.
+//
+// K order.  A 16-byte load gives lane (n, r) = (lane % 16, lane / 16) the four
+// inputs k = 16 q + 4 r .. 16 q + 4 r + 3 of its position; step t of chunk q
+// multiplies component t, so MFMA K slot r of that step is k = 16 q + 4 r + t.
+// The A fragment is read in the same order.
+#include <stdio.h>
+
+#include <algorithm>
+
+#include "common.hpp"
+#include "epilogue.hpp"
+
+namespace cliff {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned u4 __attribute__((ext_vector_type(4)));
+
+struct LinArgs {
+    const float* x;
+    const float* w;
+    const float* bias;
+    float* y;
+    int64_t B;     // positions (rows of X and Y)
+    int64_t n_wt;  // wave tiles: ceil(B / (16 NWW))
+    int C_in;
+    int WP;        // LDS floats per input channel of the weight (N plus padding)
+    SignMasks sign;
+    ActParams act;
+};
+
+// NB blades; RT = N / 16 row tiles (all of them per wave); KQ = K / 16
+// chunks; NWW 16-position column tiles per wave tile; PF chunks of prefetch.
+// Measured on MI355X (interleaved timing, C = 32 layers): 16 accumulator
+// tiles per wave at 2 waves per SIMD beat 32 tiles at 1 wave by 2-11 %; 8
+// chunks of prefetch are within noise of 4; non-temporal input loads cost
+// 2-30 %.
+#ifndef CLIFF_LIN_CHAINS  // accumulator tiles per wave
+#define CLIFF_LIN_CHAINS 16
+#endif
+#ifndef CLIFF_LIN_PF  // chunks of 16 K values prefetched ahead
+#define CLIFF_LIN_PF 4
+#endif
+#ifndef CLIFF_LIN_WAVES  // waves per SIMD the registers are sized for
+#define CLIFF_LIN_WAVES 2
+#endif
+
+template <int NB, int RT, int KQ, int NWW, int PF>
+__global__ __launch_bounds__(256, CLIFF_LIN_WAVES) void linear_mfma_kernel(LinArgs a)
+{
+    static_assert(KQ % PF == 0 && KQ >= PF, "whole prefetch rounds per tile");
+    constexpr int N = 16 * RT;
+    constexpr int TP = 16 * NWW;
+    extern __shared__ f4 smem4[];
+    float* wl = reinterpret_cast<float*>(smem4);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int waves = blockDim.x >> 6;
+    const int n = lane & 15, r = lane >> 4;
+    constexpr int K = KQ * 16;
+    const int WP = a.WP;
+    const int QS = (16 / NB) * WP;  // LDS floats per K chunk (16 / NB channels)
+
+    // LDS: the raw weight [C_in][N] in rows of WP floats; then the bias [N]
+    // (zero without one), each (co, blade)'s gate coefficient [N] and each
+    // channel's gate bias [N / N_B] (Linear mode; zero otherwise).  The
+    // epilogue reads them from here: a global load issued after the input
+    // prefetch would have to wait for all of it.
+    float* bl = wl + a.C_in * WP;
+    float* cl = bl + N;
+    float* gl = cl + N;
+    for (int e = tid; e < a.C_in * (N / 4); e += blockDim.x) {
+        const int ci = e / (N / 4), c4 = e - ci * (N / 4);
+        *reinterpret_cast<f4*>(wl + ci * WP + c4 * 4) =
+            *reinterpret_cast<const f4*>(a.w + (int64_t)e * 4);
+    }
+    for (int e = tid; e < N; e += blockDim.x) {
+        bl[e] = a.bias ? a.bias[e] : 0.f;
+        cl[e] = a.act.mode >= 0 ? gate_coef(a.act, gate_slot(a.act, e % NB), e / NB) : 0.f;
+        if (e < N / NB) gl[e] = a.act.mode == CLIFF_AGG_LINEAR ? a.act.bias[e] : 0.f;
+    }
+    __syncthreads();
+
+    // A fragment lane (row n of a row tile, K slot r): row = (co, i) with
+    // i = n % NB; step t reads input channel (4 r + t) / NB of the chunk and
+    // blade j = (4 r + t) % NB, i.e. weight blade src(i, j) with sign s(i, j).
+    const int i = n % NB;
+    int abase[4];
+    float sg[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int k0 = 4 * r + t, ci0 = k0 / NB, j = k0 % NB;
+        abase[t] = ci0 * WP + (n - i) + src_blade(NB, i, j);
+        sg[t] = sign_of(a.sign, i * NB + j);
+    }
+
+    const int64_t stride = (int64_t)gridDim.x * waves;
+    int64_t t = (int64_t)blockIdx.x * waves + wave;
+    if (t >= a.n_wt) return;  // wave-uniform, after the only barrier
+    // row of X for column tile nw of wave tile tt (past B: the last row,
+    // loaded but never stored)
+    auto xrow = [&](int64_t tt, int nw) {
+        const int64_t m = tt * TP + nw * 16 + n;
+        return a.x + (m < a.B ? m : a.B - 1) * K + 4 * r;
+    };
+    f4 ring[PF][NWW];
+#pragma unroll
+    for (int p = 0; p < PF; ++p)
+#pragma unroll
+        for (int nw = 0; nw < NWW; ++nw)
+            ring[p][nw] = *reinterpret_cast<const f4*>(xrow(t, nw) + p * 16);
+    // A values of the next step, read one step ahead
+    float fa[2][RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) fa[0][rt] = wl[abase[0] + 16 * rt];
+
+    // One tile's K loop, fully unrolled (KQ is a compile-time constant), so
+    // that the compiler's wait counts stay exact: at a loop header it would
+    // have to assume the oldest state of every edge and, with the previous
+    // tile's stores issued after the prefetch, wait for those stores too.
+    f4 acc[RT][NWW];
+    auto tile = [&](int64_t tt, int64_t tnext) {
+        const float* xc[NWW];
+        const float* xn[NWW];
+#pragma unroll
+        for (int nw = 0; nw < NWW; ++nw) {
+            xc[nw] = xrow(tt, nw);
+            xn[nw] = xrow(tnext, nw);
+        }
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int nw = 0; nw < NWW; ++nw) acc[rt][nw] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4 * KQ; ++s) {
+            const int q = s / 4, st = s % 4, cur = s & 1, p = q % PF;
+            // this step's signed A values, then the next step's A reads
+            // (step 0 of the next tile after the last) spread between this
+            // step's MFMAs, so their LDS latency is hidden
+            float as[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) as[rt] = fa[cur][rt] * sg[st];
+            const int s1 = (s + 1) % (4 * KQ);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                fa[cur ^ 1][rt] = wl[abase[s1 % 4] + (s1 / 4) * QS + 16 * rt];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int nw = 0; nw < NWW; ++nw)
+                    acc[rt][nw] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        as[rt], ring[p][nw][st], acc[rt][nw], 0, 0, 0);
+            if (st == 3) {
+                // refill slot p: chunk q + PF of this tile, or chunk
+                // q + PF - KQ of the next one (of this one again after the
+                // last tile: a harmless reload)
+#pragma unroll
+                for (int nw = 0; nw < NWW; ++nw) {
+                    const float* src =
+                        q + PF < KQ ? xc[nw] + (q + PF) * 16 : xn[nw] + (q + PF - KQ) * 16;
+                    ring[p][nw] = *reinterpret_cast<const f4*>(src);
+                }
+            }
+            __builtin_amdgcn_sched_group_barrier(0x002, RT, 0);  // sign multiplies
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                __builtin_amdgcn_sched_group_barrier(0x008, NWW, 0);  // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, RT * NWW, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, NWW, 0);      // global loads
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    int64_t tn = t + stride;
+    tile(t, tn < a.n_wt ? tn : t);
+    for (;;) {
+        const bool has_next = tn < a.n_wt;
+        // Epilogue: D fragment lane (n, r) holds rows 4 r .. 4 r + 3 of each
+        // row tile for position column n: bias, optional activation, one
+        // 16-byte store per tile (the stores drain during the next tile).
+        // The bias and gate parameters are the same for every tile; an opaque
+        // zero offset keeps their LDS reads here instead of in registers
+        // across the tile loop.
+        int opq = 0;
+        __asm__ volatile("" : "+s"(opq));
+        const float* ble = bl + opq;
+        const float* cle = cl + opq;
+        const float* gle = gl + opq;
+        const bool has_act = a.act.mode >= 0;
+        const bool mean = a.act.mode == CLIFF_AGG_MEAN;
+        // Stores go through a buffer descriptor covering this tile's valid
+        // rows: the hardware drops those past B, with no branch (a branch
+        // around a store would make the compiler assume the store might not
+        // have been issued and wait for the next tile's prefetch too early).
+        const int64_t m0 = t * TP;
+        const int64_t rows = a.B - m0 < TP ? a.B - m0 : TP;
+        const __amdgpu_buffer_rsrc_t ydesc = __builtin_amdgcn_make_buffer_rsrc(
+            a.y + m0 * N, (short)0, (int)(rows * N * 4), 0x00020000);
+        // sigmoid of the gate: Linear adds the channel's bias (zero in the
+        // other modes), Mean divides by the number of blades
+        auto gate = [&](float sum, int co) {
+            float s = sum + gle[co];
+            if (mean) s = s / (float)a.act.K;
+            return 1.0f / (1.0f + __expf(-s));
+        };
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const int row0 = 16 * rt + 4 * r;  // = co * NB + blade of component 0
+            const f4 bb = *reinterpret_cast<const f4*>(ble + row0);
+            f4 cf = f4{0.f, 0.f, 0.f, 0.f};
+            if (has_act) cf = *reinterpret_cast<const f4*>(cle + row0);
+#pragma unroll
+            for (int nw = 0; nw < NWW; ++nw) {
+                f4 v = acc[rt][nw] + bb;
+                if (has_act) {
+                    if constexpr (NB == 2) {
+                        // two multivectors: channels row0 / 2 and row0 / 2 + 1
+                        const float g0 = gate(cf[0] * v[0] + cf[1] * v[1], row0 / 2);
+                        const float g1 = gate(cf[2] * v[2] + cf[3] * v[3], row0 / 2 + 1);
+                        v[0] *= g0;
+                        v[1] *= g0;
+                        v[2] *= g1;
+                        v[3] *= g1;
+                    } else {
+                        float part = cf[0] * v[0] + cf[1] * v[1] + cf[2] * v[2] + cf[3] * v[3];
+                        // N_B = 8: the other half of the multivector is in lane ^ 16
+                        if (NB == 8) part += __shfl_xor(part, 16);
+                        v *= gate(part, row0 / NB);
+                    }
+                }
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), ydesc,
+                                                       ((nw * 16 + n) * N + row0) * 4, 0, 0);
+            }
+        }
+        if (!has_next) break;
+        t = tn;
+        tn = t + stride;
+        tile(t, tn < a.n_wt ? tn : t);
+    }
+}
+
+int device_cus()
+{
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cus[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cus[dev] = v;
+    }
+    return cus[dev];
+}
+
+template <int NB, int RT, int KQ>
+cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
+{
+    // 16 independent accumulator tiles per wave
+    constexpr int NWW = RT >= CLIFF_LIN_CHAINS ? 1 : CLIFF_LIN_CHAINS / RT;
+    constexpr int PF = CLIFF_LIN_PF < KQ ? CLIFF_LIN_PF : KQ;
+    constexpr int TP = 16 * NWW;
+    constexpr int N = 16 * RT;
+    if (p.C_out * NB != N || p.C_in * NB != 16 * KQ) return CLIFF_EUNSUPPORTED;
+    // LDS pitch: the four K slots of an A read fall on different banks
+    const int want = NB == 2 ? 8 : 16;
+    const int WP = N + ((want - N % 64) % 64 + 64) % 64;
+    const int64_t lds = (p.C_in * (int64_t)WP + 2 * N + N / NB) * 4;
+    if (lds > 160 * 1024) return CLIFF_EUNSUPPORTED;
+    const int64_t n_wt = (p.B + TP - 1) / TP;
+    if (n_wt >= (1ll << 40)) return CLIFF_EUNSUPPORTED;
+    auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF>;
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, (size_t)lds) != hipSuccess ||
+        occ < 1)
+        return CLIFF_EUNSUPPORTED;
+    const int cus = device_cus();
+    if (cus < 1) return CLIFF_EDEVICE;
+    const int64_t n_wg = std::min<int64_t>((n_wt + 3) / 4, (int64_t)cus * occ);
+
+    LinArgs a;
+    a.x = p.x;
+    a.w = p.w;
+    a.bias = p.bias;
+    a.y = p.y;
+    a.B = p.B;
+    a.n_wt = n_wt;
+    a.C_in = (int)p.C_in;
+    a.WP = WP;
+    a.sign = p.sign;
+    a.act = p.act;
+    if (debug_enabled())
+        fprintf(stderr,
+                "cliffconv: linear_mfma N_B=%d N=%d K=%d, %d positions per wave tile, "
+                "%lld wave tiles, %lld workgroups (%d per CU), %lld LDS bytes\n",
+                NB, N, 16 * KQ, TP, (long long)n_wt, (long long)n_wg, occ, (long long)lds);
+    hipLaunchKernelGGL(kern, dim3((unsigned)n_wg), dim3(256), (size_t)lds, stream, a);
+    return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
+}
+
+}  // namespace
+
+// Square layers (C_in = C_out) with C_out N_B = 64, 128 or 256, i.e. 32, 64 or
+// 128 channels (k = 1), 16, 32 or 64 (k = 2), 8, 16 or 32 (k = 3).
+cliff_status launch_linear_mfma(const ConvProblem& p, hipStream_t stream)
+{
+    if (p.d_image != 1 || p.d_filter != 1 || p.C_in != p.C_out) return CLIFF_EUNSUPPORTED;
+    const int64_t N = p.C_out * p.nb;
+    switch (p.nb) {
+        case 2:
+            if (N == 64) return run_linear<2, 4, 4>(p, stream);
+            if (N == 128) return run_linear<2, 8, 8>(p, stream);
+            if (N == 256) return run_linear<2, 16, 16>(p, stream);
+            break;
+        case 4:
+            if (N == 64) return run_linear<4, 4, 4>(p, stream);
+            if (N == 128) return run_linear<4, 8, 8>(p, stream);
+            if (N == 256) return run_linear<4, 16, 16>(p, stream);
+            break;
+        case 8:
+            if (N == 64) return run_linear<8, 4, 4>(p, stream);
+            if (N == 128) return run_linear<8, 8, 8>(p, stream);
+            if (N == 256) return run_linear<8, 16, 16>(p, stream);
+            break;
+    }
+    return CLIFF_EUNSUPPORTED;
+}
+
+}  // namespace cliff

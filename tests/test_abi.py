@@ -224,7 +224,7 @@ def test_block_zero_batch_is_noop(no_gpu):
 
 def test_bad_algo(no_gpu):
     st = P.clifford_conv_nd_algo(2, (1, 1), 2, 3, 4, 8, 3, FAKE, FAKE + (1 << 24),
-                                 FAKE + (2 << 24), FAKE + (3 << 24), None, 0, 7)
+                                 FAKE + (2 << 24), FAKE + (3 << 24), None, 0, 8)
     assert st == P.CLIFF_EINVAL
 
 
@@ -245,3 +245,11 @@ def test_missing_library_fails_loudly(tmp_path):
             P.load(str(tmp_path / "nope.so"))
     finally:
         P._lib = saved
+
+
+def test_stream_algo_refuses_convolution(no_gpu):
+    # the streamed kernel is for linear layers only: refused before any launch
+    st = P.clifford_conv_nd_algo(2, (1, 1), 2, 32, 32, 8, 3, FAKE, FAKE + (1 << 24),
+                                 FAKE + (2 << 24), FAKE + (3 << 24), None, 0,
+                                 P.ALGO_MFMA_STREAM)
+    assert st == P.CLIFF_EUNSUPPORTED

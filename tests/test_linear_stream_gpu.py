@@ -1,0 +1,148 @@
+"""GPU parity of the streamed linear-layer kernel (Algorithm 2), forced with
+CLIFF_ALGO_MFMA_STREAM and reached through clifford_linear's automatic
+choice, against the fp64 oracle.
+
+The kernel keeps the raw weight in LDS, gives each wave whole 16-64 position
+tiles and prefetches the input across tile boundaries, so the cases cover:
+every blade count and every supported width (C_out N_B = 64, 128, 256), one
+tile and a ragged last tile, more tiles than waves (each wave then runs
+several tiles and prefetches into the next; checked on sampled rows, which
+the oracle computes exactly since rows are independent), every activation
+mode, and that rows past B are never written.  Tolerance as in the other
+parity tests: 1e-4 normwise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2507_01040_amd as P
+from gpu_util import assert_parity, dev
+from workloads import AGG_LINEAR, AGG_MEAN, AGG_SUM
+
+pytestmark = pytest.mark.gpu
+
+# (g, channels): C_out N_B = 64, 128, 256 for each blade count
+WIDTHS = [((-1,), 32), ((-1,), 64), ((-1,), 128),
+          ((1, 1), 16), ((1, -1), 32), ((-1, -1), 64),
+          ((1, 1, 1), 8), ((1, -1, 0), 16), ((-1, -1, -1), 32)]
+
+
+def _inputs(seed, B, C, nb):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, C, nb)).astype(np.float32)
+    w = rng.uniform(-1 / np.sqrt(C * nb), 1 / np.sqrt(C * nb), (C, C, nb)).astype(np.float32)
+    b = rng.standard_normal((C, nb)).astype(np.float32)
+    return x, w, b
+
+
+def _act(seed, C, mode, blades):
+    rng = np.random.default_rng(seed)
+    if mode != AGG_LINEAR:
+        return None, None
+    return (rng.standard_normal((C, len(blades))).astype(np.float32),
+            (0.1 * rng.standard_normal(C)).astype(np.float32))
+
+
+def _run(g, x, w, b, act=None, algo=P.ALGO_MFMA_STREAM, guard=0):
+    """Layer on the GPU through the C ABI; the output buffer has `guard`
+    NaN rows past B, returned separately."""
+    k = len(g)
+    B, C_in, nb = x.shape
+    C_out = w.shape[1]
+    xt, wt = dev(x), dev(w)
+    bt = dev(b) if b is not None else None
+    out = torch.full(((B + guard) * C_out * nb,), float("nan"), dtype=torch.float32,
+                     device="cuda:0")
+    desc, keep = None, []
+    if act is not None:
+        mode, blades, aw, ab = act
+        awt = dev(aw) if aw is not None else None
+        abt = dev(ab) if ab is not None else None
+        keep += [awt, abt]
+        desc = P.make_act_desc(mode, blades, awt.data_ptr() if awt is not None else 0,
+                               abt.data_ptr() if abt is not None else 0)
+    st = P.clifford_conv_nd_algo(k, g, B, C_in, C_out, 1, 1, xt.data_ptr(), wt.data_ptr(),
+                                 bt.data_ptr() if bt is not None else 0, out.data_ptr(), desc,
+                                 int(torch.cuda.current_stream().cuda_stream), algo)
+    torch.cuda.synchronize()
+    assert st == P.CLIFF_OK, P.STATUS_NAMES.get(st, st)
+    o = out.cpu().numpy()
+    n = B * C_out * nb
+    return o[:n].reshape(B, C_out, nb), o[n:]
+
+
+@pytest.mark.parametrize("g,C", WIDTHS, ids=str)
+@pytest.mark.parametrize("B", [1, 17, 1000])
+def test_stream_linear_parity(g, C, B):
+    nb = 1 << len(g)
+    x, w, b = _inputs(500 + B + C, B, C, nb)
+    y, tail = _run(g, x, w, b, guard=70)
+    assert_parity(y, oracle.linear(x, w, b, g))
+    assert np.isnan(tail).all(), "rows past B were written"
+
+
+@pytest.mark.parametrize("g,C", WIDTHS, ids=str)
+def test_stream_linear_many_tiles_per_wave(g, C):
+    # more wave tiles than the grid has waves: every wave runs several tiles
+    # and prefetches across their boundaries; ragged last tile
+    nb = 1 << len(g)
+    B = (1 << 20) // (C * nb // 32) + 13
+    x, w, b = _inputs(600 + C, B, C, nb)
+    y, tail = _run(g, x, w, b, guard=70)
+    assert np.isnan(tail).all(), "rows past B were written"
+    assert np.isfinite(y).all()
+    rng = np.random.default_rng(C)
+    rows = np.unique(np.concatenate([np.arange(64), np.arange(B - 80, B),
+                                     rng.integers(0, B, 512)]))
+    assert_parity(y[rows], oracle.linear(x[rows], w, b, g))
+
+
+ACTS = [(AGG_LINEAR, None), (AGG_SUM, (0, 1)), (AGG_MEAN, None)]
+
+
+@pytest.mark.parametrize("g,C", [((-1,), 64), ((1, -1), 32), ((1, 1, 1), 32)], ids=str)
+@pytest.mark.parametrize("mode,blades", ACTS, ids=["linear", "sum01", "mean"])
+def test_stream_linear_fused_act(g, C, mode, blades):
+    nb = 1 << len(g)
+    blades = tuple(range(nb)) if blades is None else blades
+    B = 333
+    x, w, b = _inputs(700 + C, B, C, nb)
+    aw, ab = _act(701, C, mode, blades)
+    y, _ = _run(g, x, w, b, act=(mode, blades, aw, ab))
+    ref = oracle.linear(x, w, b, g)
+    ref = oracle.act(ref[:, :, None, :], mode, blades, aw, ab)[:, :, 0, :]
+    assert_parity(y, ref)
+
+
+def test_stream_linear_no_bias():
+    g = (1, 1)
+    x, w, _ = _inputs(800, 100, 32, 4)
+    y, _ = _run(g, x, w, None)
+    assert_parity(y, oracle.linear(x, w, np.zeros((32, 4), np.float32), g))
+
+
+def test_auto_choice_matches_forced_stream():
+    # clifford_linear picks the streamed kernel for this size; both runs must
+    # be bit-identical (same kernel, no atomics)
+    g = (1, 1)
+    x, w, b = _inputs(900, 40000, 32, 4)
+    y1, _ = _run(g, x, w, b, algo=P.ALGO_MFMA_STREAM)
+    y2, _ = _run(g, x, w, b, algo=P.ALGO_AUTO)
+    assert np.array_equal(y1, y2)
+    rows = np.arange(0, 40000, 97)
+    assert_parity(y1[rows], oracle.linear(x[rows], w, b, g))
+
+
+@pytest.mark.parametrize("case", ["conv", "rect", "width"])
+def test_stream_refuses_unsupported(case):
+    g = (1, 1)
+    C_in, C_out, d = {"conv": (32, 32, 3), "rect": (32, 16, 1), "width": (24, 24, 1)}[case]
+    B = 4
+    x = dev(np.zeros((B, C_in) + (d, d) + (4,), np.float32))
+    w = dev(np.zeros((C_in, C_out, d, d, 4), np.float32))
+    out = torch.zeros(B * C_out * 4, dtype=torch.float32, device="cuda:0")
+    st = P.clifford_conv_nd_algo(2, g, B, C_in, C_out, d, d, x.data_ptr(), w.data_ptr(), 0,
+                                 out.data_ptr(), None, 0, P.ALGO_MFMA_STREAM)
+    torch.cuda.synchronize()
+    assert st == P.CLIFF_EUNSUPPORTED
