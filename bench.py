@@ -118,9 +118,7 @@ class Runner:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
             self.step()
-        for _ in range(warmup):
-            graph.replay()
-        torch.cuda.synchronize()
+        warm(graph.replay, warmup, torch)
         t0 = time.perf_counter()
         for _ in range(steps):
             graph.replay()
@@ -129,9 +127,7 @@ class Runner:
 
     def time(self, steps: int, warmup: int):
         torch = self.torch
-        for _ in range(warmup):
-            self.step()
-        torch.cuda.synchronize()
+        warm(self.step, warmup, torch)
         n_l = 1 if self.w.entry == "block2" else len(self.layers)
         ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(n_l)] for _ in range(steps)]
@@ -176,6 +172,24 @@ def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
 def _flops(x) -> int:
     """Useful FLOPs of a layer (ConvShape) or of a whole workload."""
     return x.useful_flops if isinstance(x, W.Workload) else x.useful_flops()
+
+
+# The GPU clock ramps up over the first ~25 ms of sustained work (measured on
+# MI355X: the 2D C=64 layer takes 1.29 ms on its first launches and 1.09 ms
+# from about the 20th on, again after each idle gap), so every timed region
+# follows its W warm-up steps and at least this much further work.
+MIN_WARM_S = 0.05
+
+
+def warm(fn, warmup: int, torch):
+    """W calls of fn, then more until MIN_WARM_S of wall time has passed."""
+    t0 = time.perf_counter()
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    while time.perf_counter() - t0 < MIN_WARM_S:
+        fn()
+        torch.cuda.synchronize()
 
 
 def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False):
@@ -282,8 +296,8 @@ def measure_act(nb: int, B: int, C: int, Pn: int, mode: int, blades, steps: int 
     desc = P.make_act_desc(mode, blades, aw.data_ptr(), ab.data_ptr())
     stream = torch.cuda.current_stream().cuda_stream
     call = lambda: P.multivector_act(nb, B, C, Pn, desc, x.data_ptr(), y.data_ptr(), stream)
-    for _ in range(warmup):
-        assert call() == P.CLIFF_OK
+    assert call() == P.CLIFF_OK
+    warm(call, warmup, torch)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     for e0, e1 in ev:
@@ -320,8 +334,7 @@ def measure_linear(k: int, B: int, C: int, steps: int = 30, warmup: int = 10):
     w = torch.rand((C, C, nb), device="cuda:0", generator=gen) / C
     b = torch.randn((C, nb), device="cuda:0", generator=gen)
     out = torch.empty((B, C, nb), device="cuda:0")
-    for _ in range(warmup):
-        P.linear(x, w, b, g, out=out)
+    warm(lambda: P.linear(x, w, b, g, out=out), warmup, torch)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     for e0, e1 in ev:
@@ -383,6 +396,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_min_s": MIN_WARM_S,
         "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",

@@ -1,6 +1,7 @@
 // C ABI of libcliffconv: argument checks, the signature-driven sign table and
 // kernel dispatch.  No device memory is allocated here; every call only
 // enqueues kernels on the caller's stream.
+#include <atomic>
 #include <stdint.h>
 #include <stdlib.h>
 
@@ -18,6 +19,20 @@ bool debug_enabled()
         return v && v[0] && !(v[0] == '0' && v[1] == 0);
     }();
     return on;
+}
+
+int device_cus()
+{
+    static std::atomic<int> cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int c = cus[dev].load(std::memory_order_relaxed);
+    if (c == 0) {
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cus[dev].store(c, std::memory_order_relaxed);
+    }
+    return c;
 }
 
 }  // namespace cliff

@@ -75,6 +75,9 @@ struct BlockProblem {
 // non-zero value, every launch prints its kernel, grid and tiling to stderr.
 bool debug_enabled();
 
+// Compute units of the current device (cached per device); 0 on error.
+int device_cus();
+
 // host-side launchers (defined in the .hip files)
 cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);
 // Returns CLIFF_EUNSUPPORTED without launching when no MFMA tiling fits.

@@ -259,20 +259,6 @@ __global__ __launch_bounds__(256, CLIFF_LIN_WAVES) void linear_mfma_kernel(LinAr
     }
 }
 
-int device_cus()
-{
-    static int cus[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cus[dev] == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return 0;
-        cus[dev] = v;
-    }
-    return cus[dev];
-}
-
 template <int NB, int RT, int KQ>
 cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
 {
