@@ -182,13 +182,16 @@ MIN_WARM_S = 0.05
 
 
 def warm(fn, warmup: int, torch):
-    """W calls of fn, then more until MIN_WARM_S of wall time has passed."""
+    """W calls of fn, then more until MIN_WARM_S of wall time has passed.  The
+    calls are enqueued back to back (a synchronisation every 16), so the GPU
+    stays busy: an idle GPU lowers its clock again."""
     t0 = time.perf_counter()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     while time.perf_counter() - t0 < MIN_WARM_S:
-        fn()
+        for _ in range(16):
+            fn()
         torch.cuda.synchronize()
 
 
