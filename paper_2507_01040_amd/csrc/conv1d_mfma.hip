@@ -38,6 +38,9 @@
 #ifndef CLIFF_W1  // wide tile: WCO, WPOS, MW, NW, input slots
 #define CLIFF_W1 2, 2, 4, 4, 8
 #endif
+#ifndef CLIFF_X16  // 16-byte input staging when d_image and C_out are even
+#define CLIFF_X16 1
+#endif
 #ifndef CLIFF_W1_WAVES  // wide tile: waves per SIMD the registers are sized for
 #define CLIFF_W1_WAVES 2   // (d_filter 17: 3, measured +2 %; d_filter 3: 2, 3 is -2 %)
 #endif
@@ -65,7 +68,8 @@ struct C1Args {
     ActParams act;
 };
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int WK>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int FX,
+          int WK>
 __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kernel(C1Args a)
 {
     // WK > 1: WK waves share every output tile, each taking every WK-th
@@ -96,15 +100,20 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     const int m_end = min(m0 + P, a.M);
     const int co0 = co_blk * CO_WG;
     const int b0 = m0 / Do;
-    const int x_first = m0 - b0 * Do;
+    // FX = 4 (16-byte input loads, d_image even): the window starts at an
+    // even position, so that every 16-byte piece (two positions) lies inside
+    // one batch entry and is 16-byte aligned in HBM
+    const int x_first = FX == 4 ? (m0 - b0 * Do) & ~1 : m0 - b0 * Do;
     const int b1 = (m_end - 1) / Do;
     // window length in positions: (b1 - b0) D + x_last + d_filter - x_first
     const int span = (b1 - b0) * D + (m_end - 1 - b1 * Do) + df - x_first;
 
     // Stage buffer (floats): ccp channel windows [ccp][span2], then ccp
-    // channels of filters [ccp][co][tap][2].  Input slot t of this lane is
-    // window float f = t * NT + tid (4-byte direct loads: lane i lands at
-    // base + 4 i).  Filter slot t covers filter floats FW * (t * NT + tid)
+    // channels of filters [ccp][co][tap][2].  Input slot t of this lane covers
+    // window floats FX * (t * NT + tid) onwards (direct loads: lane i lands at
+    // base + 4 FX i): FX = 4 loads two positions at once when d_image is even
+    // (span2 is then a multiple of 4), FX = 1 one float, which needs no
+    // alignment.  Filter slot t covers filter floats FW * (t * NT + tid)
     // onwards: FW = 4 (16-byte loads) when C_out is even, since then every
     // channel's chunk of CO_WG x d_filter filters is 16-byte aligned and its
     // valid part a whole number of 16-byte pieces; FW = 1 otherwise.  The
@@ -115,12 +124,21 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     uint32_t xoffb[SIN], woffb[SW];
 #pragma unroll
     for (int t = 0; t < SIN; ++t) {
-        const int f = t * NT + tid;
+        const int f = (t * NT + tid) * FX;
         const int c_l = f / span2;
         const int r = f - c_l * span2;
-        const int v = x_first + min(r / NB, span - 1);  // past the window: unused
-        const int bb = v / D;
-        xoffb[t] = 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
+        if constexpr (FX == 4) {
+            // an even position; past the window (unused) the last even one,
+            // whose pair is still inside its batch entry (d_image even)
+            const int v = x_first + min(r / NB, (span - 1) & ~1);
+            const int bb = v / D;
+            xoffb[t] = 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB);
+        } else {
+            const int v = x_first + min(r / NB, span - 1);  // past the window: unused
+            const int bb = v / D;
+            xoffb[t] =
+                4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
+        }
     }
     // filter floats of a channel chunk that belong to channels < C_out
     const int wvalid = min(CO_WG, a.C_out - co0) * df * NB;
@@ -150,13 +168,18 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
         const int nv = stage_channels(s);
         const char* xs = xbase + (int64_t)ci0 * D * NB * 4;
         const char* ws = wbase + (int64_t)ci0 * a.C_out * df * NB * 4;
-        float* lx = smem + buf * a.stage_floats + wave_u * 64;
+        float* lx = smem + buf * a.stage_floats + wave_u * 64 * FX;
         float* lw = smem + buf * a.stage_floats + w_lds + wave_u * 64 * FW;
 #pragma unroll
         for (int t = 0; t < SIN; ++t) {
-            if (t * NT + tid < nv * span2)
-                __builtin_amdgcn_global_load_lds(
-                    xs + xoffb[t], (__attribute__((address_space(3))) void*)(lx + t * NT), 4, 0, 0);
+            if ((t * NT + tid) * FX < nv * span2) {
+                auto* dst = (__attribute__((address_space(3))) void*)(lx + t * NT * FX);
+                const float* src = reinterpret_cast<const float*>(xs + xoffb[t]);
+                if constexpr (FX == 4)
+                    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+                else
+                    __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
+            }
         }
 #pragma unroll
         for (int t = 0; t < SW; ++t) {
@@ -362,7 +385,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     }
 }
 
-template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int WK>
+template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int FX,
+          int WK>
 cliff_status run1d(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NB = 2;
@@ -376,15 +400,19 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     const int64_t n_blk = n_pblk * n_co_blk;
     // P consecutive flattened positions touch at most rows_max batch entries
     const int64_t rows_max = std::min<int64_t>(p.B, (P + Do - 2) / Do + 1);
-    const int64_t span_max = P + rows_max * (df - 1);
-    const int64_t ch_floats = span_max * NB + CO_WG * df * NB;
+    // (FX = 4: one more position, the window starting at an even one, and a
+    // whole number of 16-byte pieces per channel)
+    if (FX == 4 && D % 2 != 0) return CLIFF_EUNSUPPORTED;
+    const int64_t span_max = P + rows_max * (df - 1) + (FX == 4 ? 1 : 0);
+    const int64_t span2 = FX == 4 ? (span_max * NB + 3) / 4 * 4 : span_max * NB;
+    const int64_t ch_floats = span2 + CO_WG * df * NB;
     // LDS: two stage buffers per workgroup, WAVES waves per SIMD resident
     const int64_t wg_per_cu = std::max<int64_t>(1, 4 * WAVES / (WCO * WPOS * WK));
     const int64_t lds_budget = std::min<int64_t>(CLIFF_LDS1, 160 * 1024 / wg_per_cu);
     const int64_t mfma_per_pair = df * MW * NW;
     int64_t ccp = 2 * std::max<int64_t>(1, (512 + mfma_per_pair - 1) / mfma_per_pair);
     ccp = std::min<int64_t>(ccp, (lds_budget / (2 * ch_floats * 4)) & ~int64_t(1));
-    ccp = std::min<int64_t>(ccp, ((int64_t)SIN * NT / (span_max * NB)) & ~int64_t(1));
+    ccp = std::min<int64_t>(ccp, ((int64_t)SIN * NT * FX / span2) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, ((int64_t)SW * NT * FW / (CO_WG * df * NB)) & ~int64_t(1));
     ccp = std::min<int64_t>(ccp, (p.C_in + 1) & ~int64_t(1));
     if (WK > 1 && ccp > 2 * WK) ccp -= ccp % (2 * WK);  // equal pair shares for the K slices
@@ -413,7 +441,7 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     a.cc = (int)cc;
     a.ccp = (int)ccp;
     a.n_stage = (int)((p.C_in + cc - 1) / cc);
-    a.span2 = (int)(span_max * NB);
+    a.span2 = (int)span2;
     a.stage_floats = (int)stage_floats;
     a.sign = p.sign;
     a.act = p.act;
@@ -421,21 +449,27 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
         fprintf(stderr,
                 "cliffconv: conv1d_mfma d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
                 "(%d channels x %d positions), %lld workgroups, %d channels/stage, "
-                "%lld LDS bytes, %d-byte filter loads\n",
+                "%lld LDS bytes, %d-byte input and %d-byte filter loads\n",
                 (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
-                (long long)lds_bytes, 4 * FW);
-    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, WK>),
+                (long long)lds_bytes, 4 * FX, 4 * FW);
+    hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, FX, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
 
-// 16-byte filter loads (fewer slots) when C_out is even, else 4-byte loads.
+// 16-byte filter loads (fewer slots) when C_out is even, and then also
+// 16-byte input loads when d_image is even; 4-byte loads otherwise.
 template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW1, int SW4, int WAVES,
           int WK = 1>
 cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
 {
-    if (p.C_out % 2 == 0) return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4, WK>(p, stream);
-    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, WAVES, 1, WK>(p, stream);
+    constexpr int SIN4 = (SIN + 3) / 4 + 1;  // 16-byte input slots (one more position)
+    if (p.C_out % 2 == 0 && p.d_image % 2 == 0 && CLIFF_X16)
+        return run1d<DF, WCO, WPOS, MW, NW, SIN4, SW4, WAVES, 4, 4, WK>(p, stream);
+    if (p.C_out % 2 == 0)
+        return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4, 1, WK>(p, stream);
+    // (the 4-byte filter slots need more registers: at most 2 waves per SIMD)
+    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, (WAVES < 2 ? WAVES : 2), 1, 1, WK>(p, stream);
 }
 
 // Tile shapes (waves along channels x waves along positions, MFMA tiles per

@@ -11,7 +11,8 @@ The oracle cannot afford every output at these sizes, so it checks:
   * blocks (conv -> act -> conv -> act): spatial patches; by translation
     equivariance (no padding) the block applied to a cropped input equals the
     same window of the full output, so the oracle runs the whole block, in
-    fp64 end to end, on crops at the corners, edges and interior.
+    fp64 end to end, on crops at the corners, edges and interior of every
+    batch entry.
 Gate: normwise relative error <= 1e-4 (see test_parity_gpu).
 """
 import itertools
@@ -125,7 +126,7 @@ def test_block_patches(name, ps):
         layers.append((p.filters, p.bias,
                        None if a is None else (a.mode, a.blades, p.act_weight, p.act_bias)))
     worst = 0.0
-    for b in (0, w.layers[0].B - 1):
+    for b in range(w.layers[0].B):
         for org in _patch_origins(d_final, ps, k, b):
             crop = (slice(b, b + 1), slice(None)) + tuple(
                 slice(o, o + ps + halo) for o in org)

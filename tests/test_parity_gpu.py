@@ -58,6 +58,11 @@ SHAPES1 = [
     (1, 2, 8, 200, 5),
     (6, 39, 19, 80, 4),   # even filter, odd channel count over stages
     (64, 37, 64, 1, 1),   # linear layer
+    # even d_image and C_out (16-byte input staging) with odd d_out, so that
+    # windows start at odd positions and are widened to the even one before
+    (3, 5, 66, 60, 16),
+    (6, 39, 20, 80, 4),
+    (2, 3, 64, 20, 2),
 ]
 
 
