@@ -24,6 +24,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "common.hpp"
 #include "epilogue.hpp"
@@ -276,10 +277,17 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     const int64_t n_wt = (p.B + TP - 1) / TP;
     if (n_wt >= (1ll << 40)) return CLIFF_EUNSUPPORTED;
     auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF>;
-    int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, (size_t)lds) != hipSuccess ||
-        occ < 1)
-        return CLIFF_EUNSUPPORTED;
+    // resident workgroups per CU, cached per LDS size (packed (lds << 8) | occ)
+    static std::atomic<int64_t> occ_cache{0};
+    int64_t oc = occ_cache.load(std::memory_order_relaxed);
+    int occ = (oc >> 8) == lds ? (int)(oc & 0xff) : 0;
+    if (occ == 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, (size_t)lds) !=
+                hipSuccess ||
+            occ < 1)
+            return CLIFF_EUNSUPPORTED;
+        occ_cache.store((lds << 8) | std::min(occ, 255), std::memory_order_relaxed);
+    }
     const int cus = device_cus();
     if (cus < 1) return CLIFF_EDEVICE;
     const int64_t n_wg = std::min<int64_t>((n_wt + 3) / 4, (int64_t)cus * occ);
