@@ -8,8 +8,9 @@ every blade count and every supported width (C_out N_B = 64, 128, 256), one
 tile and a ragged last tile, more tiles than waves (each wave then runs
 several tiles and prefetches into the next; checked on sampled rows, which
 the oracle computes exactly since rows are independent), every activation
-mode, and that rows past B are never written.  Tolerance as in the other
-parity tests: 1e-4 normwise.
+mode, that rows past B are never written, and the benchmark's three linear
+layers at their full size through the automatic choice.  Tolerance as in the
+other parity tests: 1e-4 normwise.
 """
 import numpy as np
 import pytest
@@ -146,3 +147,22 @@ def test_stream_refuses_unsupported(case):
                                  out.data_ptr(), None, 0, P.ALGO_MFMA_STREAM)
     torch.cuda.synchronize()
     assert st == P.CLIFF_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("k,B", [(2, 1 << 20), (3, 1 << 19), (1, 1 << 21)], ids=str)
+def test_benchmark_linear_layers_full_size(k, B):
+    # the benchmark's linear layers (C = 32, g = (1,)*k) at their full batch,
+    # through clifford_linear's automatic choice as the benchmark calls it;
+    # checked on sampled rows (rows are independent)
+    g = (1,) * k
+    nb = 1 << k
+    C = 32
+    x, w, b = _inputs(1000 + k, B, C, nb)
+    y = P.linear(dev(x), dev(w), dev(b), g)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(k)
+    rows = np.unique(np.concatenate([np.arange(32), np.arange(B - 32, B),
+                                     rng.integers(0, B, 1024)]))
+    got = y[torch.from_numpy(rows).to(y.device)].cpu().numpy()
+    assert np.isfinite(got).all()
+    assert_parity(got, oracle.linear(x[rows], w, b, g))
