@@ -569,6 +569,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
 #endif
 #define CLIFF_W2_32 2, 2, 4, 8, 6, 2  // k = 2 wide variant for C_out <= 32
+#define CLIFF_W3_32 4, 1, 4, 8, 6, 2  // k = 3, 3x3x3 wide variant for 16 < C_out <= 32
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
 #define CLIFF_NARROW 1, 4, 2, 4, 8, 2
@@ -611,6 +612,12 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
         if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32>>(p, stream);
         return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2>>(p, stream);
     } else {
+        // k = 3 with 3x3x3 filters and 17..32 output channels: all of them
+        // in one 32 x 128 tile (measured +0.9 % at C = 32 against two 16 x
+        // 128 blocks; with 64 channels the 16 x 128 tile stays 2 % faster)
+        if constexpr (DF == 3)
+            if (p.C_out <= 32 && p.C_out > 16)
+                return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3_32>>(p, stream);
         return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3>>(p, stream);
     }
 }

@@ -45,6 +45,8 @@ SHAPES3 = [
     (2, 2, 4, 3, 1),
     (8, 4, 4, 16, 3),     # several channels per stage
     (64, 37, 64, 1, 1),   # linear layer
+    (2, 5, 24, 10, 3),    # 16 < C_out <= 32: the 32-channel wide tile
+    (3, 6, 32, 9, 3),
 ]
 SHAPES1 = [
     (1, 1, 1, 3, 3),      # one output, one channel (odd: half of the pair is off)
