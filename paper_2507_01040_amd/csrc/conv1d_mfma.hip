@@ -44,6 +44,9 @@
 #ifndef CLIFF_W1_WAVES  // wide tile: waves per SIMD the registers are sized for
 #define CLIFF_W1_WAVES 2   // (d_filter 17: 3, measured +2 %; d_filter 3: 2, 3 is -2 %)
 #endif
+#ifndef CLIFF_W1_WAVES17
+#define CLIFF_W1_WAVES17 3
+#endif
 
 namespace cliff {
 namespace {
@@ -485,7 +488,7 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     // <DF, WCO, WPOS, MW, NW, input slots, filter slots with 4-byte and with
     // 16-byte loads, waves per SIMD>
     auto wide = [&] {
-        return run1d_fw<DF, CLIFF_W1, 18, 6, DF == 17 ? 3 : CLIFF_W1_WAVES>(p, stream);
+        return run1d_fw<DF, CLIFF_W1, 18, 6, DF == 17 ? CLIFF_W1_WAVES17 : CLIFF_W1_WAVES>(p, stream);
     };
     auto medium = [&] { return run1d_fw<DF, 2, 1, 4, 2, 8, 18, 9, 2>(p, stream); };
     auto narrow = [&] { return run1d_fw<DF, 1, 4, 1, 4, 16, 4, 2, 2>(p, stream); };
