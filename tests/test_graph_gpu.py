@@ -72,3 +72,32 @@ def test_graph_replay_block2(path):
         graph.replay()
         torch.cuda.synchronize()
         assert torch.equal(out_g, eager), "replay %d differs from eager" % rep
+
+
+def test_graph_replay_linear_stream():
+    # the streamed linear kernel (persistent grid, buffer-descriptor stores)
+    # captured and replayed, with its fused activation
+    g = (1, 1)
+    B, C = 40000, 32
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((B, C, 4)).astype(np.float32)
+    xt = dev(x)
+    wt = dev(rng.uniform(-0.1, 0.1, (C, C, 4)).astype(np.float32))
+    bt = dev(rng.standard_normal((C, 4)).astype(np.float32))
+    act = (P.AGG_SUM, (0, 3), None, None)
+    out_g = torch.empty((B, C, 4), device="cuda:0")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        P.linear(xt, wt, bt, g, act=act, out=out_g)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.linear(xt, wt, bt, g, act=act, out=out_g)
+    for rep in range(3):
+        xt.copy_(dev(x * (1.0 - 0.3 * rep)))
+        eager = P.linear(xt, wt, bt, g, act=act)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, eager), "replay %d differs from eager" % rep
