@@ -130,10 +130,10 @@ typedef enum {
     CLIFF_ALGO_MFMA_TINY = 6,   /* MFMA, 8 / 4 / 2 channels x 32 positions
                                    (k = 2, 3: the K loop split over 4 waves) */
     CLIFF_ALGO_MFMA_STREAM = 7  /* MFMA, linear layers only (d_image =
-                                   d_filter = 1, C_in = C_out, C_out N_B = 64,
-                                   128 or 256): persistent waves that stream
-                                   16-64 positions at a time past the weight
-                                   held in LDS */
+                                   d_filter = 1, C_in N_B and C_out N_B each
+                                   64, 128 or 256): persistent waves that
+                                   stream 16-64 positions at a time past the
+                                   weight held in LDS */
 } cliff_algo;
 
 /*
@@ -162,8 +162,8 @@ cliff_status clifford_conv_nd_algo(int k, const int8_t* g, int64_t B,
  *   bias      device [C_out, N_B], or NULL for zero
  *   output    device [B, C_out, N_B]; must not overlap any input
  * Same alignment, size, error and stream rules as clifford_conv_nd; it is
- * the convolution with d_image = d_filter = 1.  Square layers with
- * C_out N_B = 64, 128 or 256 and B >= 16384 run on a streamed kernel that
+ * the convolution with d_image = d_filter = 1.  Layers with C_in N_B and
+ * C_out N_B each 64, 128 or 256 and B >= 16384 run on a streamed kernel that
  * keeps the weight in LDS (CLIFF_ALGO_MFMA_STREAM); other layers on the
  * convolution kernels.
  */

@@ -265,7 +265,10 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
 {
     // 16 independent accumulator tiles per wave
     constexpr int NWW = RT >= CLIFF_LIN_CHAINS ? 1 : CLIFF_LIN_CHAINS / RT;
-    constexpr int PF = CLIFF_LIN_PF < KQ ? CLIFF_LIN_PF : KQ;
+    // (N = 64 with K = 256: 2 chunks, which keeps that unrolled kernel
+    // within the registers of 2 waves per SIMD)
+    constexpr int PF0 = CLIFF_LIN_PF < KQ ? CLIFF_LIN_PF : KQ;
+    constexpr int PF = RT == 4 && KQ == 16 && PF0 > 2 ? 2 : PF0;
     constexpr int TP = 16 * NWW;
     constexpr int N = 16 * RT;
     if (p.C_out * NB != N || p.C_in * NB != 16 * KQ) return CLIFF_EUNSUPPORTED;
@@ -312,30 +315,37 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
 
+template <int NB, int RT>
+cliff_status run_linear_k(const ConvProblem& p, hipStream_t stream, int64_t kq)
+{
+    if (kq == 4) return run_linear<NB, RT, 4>(p, stream);
+    if (kq == 8) return run_linear<NB, RT, 8>(p, stream);
+    if (kq == 16) return run_linear<NB, RT, 16>(p, stream);
+    return CLIFF_EUNSUPPORTED;
+}
+
+template <int NB>
+cliff_status run_linear_nk(const ConvProblem& p, hipStream_t stream)
+{
+    const int64_t rt = p.C_out * NB / 16, kq = p.C_in * NB / 16;
+    if (p.C_out * NB % 16 != 0 || p.C_in * NB % 16 != 0) return CLIFF_EUNSUPPORTED;
+    if (rt == 4) return run_linear_k<NB, 4>(p, stream, kq);
+    if (rt == 8) return run_linear_k<NB, 8>(p, stream, kq);
+    if (rt == 16) return run_linear_k<NB, 16>(p, stream, kq);
+    return CLIFF_EUNSUPPORTED;
+}
+
 }  // namespace
 
-// Square layers (C_in = C_out) with C_out N_B = 64, 128 or 256, i.e. 32, 64 or
-// 128 channels (k = 1), 16, 32 or 64 (k = 2), 8, 16 or 32 (k = 3).
+// Layers whose C_out N_B and C_in N_B are each 64, 128 or 256, i.e. 32, 64
+// or 128 channels (k = 1), 16, 32 or 64 (k = 2), 8, 16 or 32 (k = 3).
 cliff_status launch_linear_mfma(const ConvProblem& p, hipStream_t stream)
 {
-    if (p.d_image != 1 || p.d_filter != 1 || p.C_in != p.C_out) return CLIFF_EUNSUPPORTED;
-    const int64_t N = p.C_out * p.nb;
+    if (p.d_image != 1 || p.d_filter != 1) return CLIFF_EUNSUPPORTED;
     switch (p.nb) {
-        case 2:
-            if (N == 64) return run_linear<2, 4, 4>(p, stream);
-            if (N == 128) return run_linear<2, 8, 8>(p, stream);
-            if (N == 256) return run_linear<2, 16, 16>(p, stream);
-            break;
-        case 4:
-            if (N == 64) return run_linear<4, 4, 4>(p, stream);
-            if (N == 128) return run_linear<4, 8, 8>(p, stream);
-            if (N == 256) return run_linear<4, 16, 16>(p, stream);
-            break;
-        case 8:
-            if (N == 64) return run_linear<8, 4, 4>(p, stream);
-            if (N == 128) return run_linear<8, 8, 8>(p, stream);
-            if (N == 256) return run_linear<8, 16, 16>(p, stream);
-            break;
+        case 2: return run_linear_nk<2>(p, stream);
+        case 4: return run_linear_nk<4>(p, stream);
+        case 8: return run_linear_nk<8>(p, stream);
     }
     return CLIFF_EUNSUPPORTED;
 }

@@ -4,7 +4,8 @@ choice, against the fp64 oracle.
 
 The kernel keeps the raw weight in LDS, gives each wave whole 16-64 position
 tiles and prefetches the input across tile boundaries, so the cases cover:
-every blade count and every supported width (C_out N_B = 64, 128, 256), one
+every blade count and every supported width (C_out N_B = 64, 128, 256),
+rectangular layers (C_in N_B != C_out N_B), one
 tile and a ragged last tile, more tiles than waves (each wave then runs
 several tiles and prefetches into the next; checked on sampled rows, which
 the oracle computes exactly since rows are independent), every activation
@@ -29,11 +30,12 @@ WIDTHS = [((-1,), 32), ((-1,), 64), ((-1,), 128),
           ((1, 1, 1), 8), ((1, -1, 0), 16), ((-1, -1, -1), 32)]
 
 
-def _inputs(seed, B, C, nb):
+def _inputs(seed, B, C, nb, C_out=None):
+    C_out = C if C_out is None else C_out
     rng = np.random.default_rng(seed)
     x = rng.standard_normal((B, C, nb)).astype(np.float32)
-    w = rng.uniform(-1 / np.sqrt(C * nb), 1 / np.sqrt(C * nb), (C, C, nb)).astype(np.float32)
-    b = rng.standard_normal((C, nb)).astype(np.float32)
+    w = rng.uniform(-1 / np.sqrt(C * nb), 1 / np.sqrt(C * nb), (C, C_out, nb)).astype(np.float32)
+    b = rng.standard_normal((C_out, nb)).astype(np.float32)
     return x, w, b
 
 
@@ -99,6 +101,37 @@ def test_stream_linear_many_tiles_per_wave(g, C):
     assert_parity(y[rows], oracle.linear(x[rows], w, b, g))
 
 
+# (g, C_in, C_out) with C_in N_B != C_out N_B, both in {64, 128, 256}
+RECT = [((-1,), 32, 128), ((-1,), 128, 64),
+        ((1, 1), 16, 32), ((1, -1), 32, 16), ((1, 1), 16, 64), ((-1, -1), 64, 16),
+        ((1, 1), 32, 64), ((1, 1), 64, 32),
+        ((1, 1, 1), 8, 32), ((1, -1, 0), 32, 16)]
+
+
+@pytest.mark.parametrize("g,C_in,C_out", RECT, ids=str)
+@pytest.mark.parametrize("B", [37, 1000])
+def test_stream_linear_rectangular(g, C_in, C_out, B):
+    nb = 1 << len(g)
+    x, w, b = _inputs(520 + B + C_in + 3 * C_out, B, C_in, nb, C_out)
+    y, tail = _run(g, x, w, b, guard=70)
+    assert_parity(y, oracle.linear(x, w, b, g))
+    assert np.isnan(tail).all(), "rows past B were written"
+
+
+@pytest.mark.parametrize("g,C_in,C_out", [((1, 1), 16, 64), ((1, 1), 64, 16),
+                                          ((-1,), 128, 32)], ids=str)
+def test_stream_linear_rectangular_many_tiles(g, C_in, C_out):
+    nb = 1 << len(g)
+    B = 300001
+    x, w, b = _inputs(540 + C_in + C_out, B, C_in, nb, C_out)
+    y, tail = _run(g, x, w, b, guard=70)
+    assert np.isnan(tail).all()
+    rng = np.random.default_rng(C_in)
+    rows = np.unique(np.concatenate([np.arange(64), np.arange(B - 80, B),
+                                     rng.integers(0, B, 512)]))
+    assert_parity(y[rows], oracle.linear(x[rows], w, b, g))
+
+
 ACTS = [(AGG_LINEAR, None), (AGG_SUM, (0, 1)), (AGG_MEAN, None)]
 
 
@@ -138,7 +171,7 @@ def test_auto_choice_matches_forced_stream():
 @pytest.mark.parametrize("case", ["conv", "rect", "width"])
 def test_stream_refuses_unsupported(case):
     g = (1, 1)
-    C_in, C_out, d = {"conv": (32, 32, 3), "rect": (32, 16, 1), "width": (24, 24, 1)}[case]
+    C_in, C_out, d = {"conv": (32, 32, 3), "rect": (32, 24, 1), "width": (24, 24, 1)}[case]
     B = 4
     x = dev(np.zeros((B, C_in) + (d, d) + (4,), np.float32))
     w = dev(np.zeros((C_in, C_out, d, d, 4), np.float32))
