@@ -215,6 +215,8 @@ __global__ __launch_bounds__(256, CLIFF_LIN_WAVES) void linear_mfma_kernel(LinAr
         // have been issued and wait for the next tile's prefetch too early).
         const int64_t m0 = t * TP;
         const int64_t rows = a.B - m0 < TP ? a.B - m0 : TP;
+        // (raw descriptor: stride 0, size in bytes; word 3 = 32-bit data
+        // format, the value CDNA's buffer instructions expect for raw access)
         const __amdgpu_buffer_rsrc_t ydesc = __builtin_amdgcn_make_buffer_rsrc(
             a.y + m0 * N, (short)0, (int)(rows * N * 4), 0x00020000);
         // sigmoid of the gate: Linear adds the channel's bias (zero in the
