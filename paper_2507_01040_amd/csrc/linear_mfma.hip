@@ -60,12 +60,15 @@ struct LinArgs {
 #ifndef CLIFF_LIN_PF  // chunks of 16 K values prefetched ahead
 #define CLIFF_LIN_PF 4
 #endif
+#ifndef CLIFF_LIN_N64_WAVES4  // N = K = 64: 8 tiles per wave at 4 waves per SIMD
+#define CLIFF_LIN_N64_WAVES4 1
+#endif
 #ifndef CLIFF_LIN_WAVES  // waves per SIMD the registers are sized for
 #define CLIFF_LIN_WAVES 2
 #endif
 
-template <int NB, int RT, int KQ, int NWW, int PF>
-__global__ __launch_bounds__(256, CLIFF_LIN_WAVES) void linear_mfma_kernel(LinArgs a)
+template <int NB, int RT, int KQ, int NWW, int PF, int WAVES>
+__global__ __launch_bounds__(256, WAVES) void linear_mfma_kernel(LinArgs a)
 {
     static_assert(KQ % PF == 0 && KQ >= PF, "whole prefetch rounds per tile");
     constexpr int N = 16 * RT;
@@ -265,8 +268,13 @@ __global__ __launch_bounds__(256, CLIFF_LIN_WAVES) void linear_mfma_kernel(LinAr
 template <int NB, int RT, int KQ>
 cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
 {
-    // 16 independent accumulator tiles per wave
-    constexpr int NWW = RT >= CLIFF_LIN_CHAINS ? 1 : CLIFF_LIN_CHAINS / RT;
+    // 16 independent accumulator tiles per wave at 2 waves per SIMD; N = K =
+    // 64 (HBM-bound) does better with 8 tiles at 4 waves per SIMD, more loads
+    // in flight (measured +7 % on the 1-D C = 32 layer, -1 to -3 % at N = 128)
+    constexpr bool NARROW_N = RT == 4 && KQ == 4 && CLIFF_LIN_N64_WAVES4;
+    constexpr int CHAINS = NARROW_N ? 8 : CLIFF_LIN_CHAINS;
+    constexpr int WAVES = NARROW_N ? 4 : CLIFF_LIN_WAVES;
+    constexpr int NWW = RT >= CHAINS ? 1 : CHAINS / RT;
     // (N = 64 with K = 256: 2 chunks, which keeps that unrolled kernel
     // within the registers of 2 waves per SIMD)
     constexpr int PF0 = CLIFF_LIN_PF < KQ ? CLIFF_LIN_PF : KQ;
@@ -281,7 +289,7 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     if (lds > 160 * 1024) return CLIFF_EUNSUPPORTED;
     const int64_t n_wt = (p.B + TP - 1) / TP;
     if (n_wt >= (1ll << 40)) return CLIFF_EUNSUPPORTED;
-    auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF>;
+    auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES>;
     // resident workgroups per CU, cached per LDS size (packed (lds << 8) | occ)
     static std::atomic<int64_t> occ_cache{0};
     int64_t oc = occ_cache.load(std::memory_order_relaxed);
