@@ -18,9 +18,10 @@
 // position to its last one plus d_filter - 1, crossing entry boundaries; the
 // positions of an entry past d_out are staged too (they are the last taps of
 // that entry).  Per stage (a group of input channels, double-buffered in LDS)
-// it stages each channel's window and raw filters with 4-byte direct
-// global->LDS loads, which need no alignment (a 1-D row or filter chunk is in
-// general not 16-byte aligned).
+// it stages each channel's window and raw filters with direct global->LDS
+// loads: 16-byte ones where the layout allows (even C_out for the filters;
+// even d_image as well for the windows, which then start at an even
+// position), 4-byte ones otherwise, which need no alignment.
 #include <stdio.h>
 
 #include <algorithm>
