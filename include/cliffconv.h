@@ -3,9 +3,11 @@
  * (libcliffconv.so).
  *
  * The operations are those of "Fast Clifford Neural Layers" (arXiv
- * 2507.01040): the k-D Clifford convolution of Algorithm 1 with the bias add,
- * and the multivector activation of Algorithm 3, usable on its own or fused
- * as the convolution's epilogue.  All arithmetic is IEEE fp32 on the GPU.
+ * 2507.01040): the k-D Clifford convolution of Algorithm 1 and the Clifford
+ * linear layer of Algorithm 2, each with the bias add, the multivector
+ * activation of Algorithm 3, usable on its own or fused as their epilogue,
+ * and the two-layer block (convolution + activation, twice) the paper builds
+ * its networks from.  All arithmetic is IEEE fp32 on the GPU.
  *
  * Algebra (paper, Background, "Clifford Algebra"): Cl_g(R^k) with signature
  * g in {-1, 0, +1}^k, generators e_1..e_k, e_i e_i = g_i, e_i e_j = -e_j e_i.
