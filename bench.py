@@ -143,6 +143,15 @@ class Runner:
         return wall / steps * 1e3, per_layer_ms
 
 
+def _device_info(torch):
+    """Name, architecture and compute-unit count of the GPU the line was
+    measured on (the peaks assume 256 CUs at 2.4 GHz)."""
+    pr = torch.cuda.get_device_properties(0)
+    return {"name": pr.name, "arch": getattr(pr, "gcnArchName", None),
+            "compute_units": pr.multi_processor_count,
+            "memory_gib": round(pr.total_memory / 2 ** 30, 1)}
+
+
 def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
     """The fp64 oracle on a bounded sample: the first batch entries of the
     workload (as many as fit the time budget, at least one)."""
@@ -421,6 +430,7 @@ def main():
                      "kernel_ms": dom_ms,
                      "kernel_source_hash": kernel_source_hash()},
         "workload_detail": head,
+        "device": _device_info(torch),
     }
     if probe is not None:
         line["mfma_probe"] = probe
