@@ -123,7 +123,8 @@ typedef enum {
     CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA, tile shape chosen
                                    from the problem size */
     CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=1; k=2, or
-                                   32 x 256 when C_out <= 32) / 16 (k=3; 32
+                                   32 x 256 when C_out <= 32 or when a 64-
+                                   channel stage does not fit) / 16 (k=3; 32
                                    when 16 < C_out <= 32 and d_filter = 3)
                                    channels x 128 positions per workgroup */
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32

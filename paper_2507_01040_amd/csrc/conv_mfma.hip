@@ -475,7 +475,7 @@ struct TileCfg {
 };
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
-          int WAVES, int WK>
+          int WAVES, int WK, int LDSKB>
 cliff_status run(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NT = 64 * WCO * WPOS * WK;
@@ -499,7 +499,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     const int64_t ch_floats = rows_max * D * NB + CO_WG * df * df * NB;  // per channel
     // Channels per stage: enough MFMAs per wave between barriers, within the
     // LDS budget (two buffers) and the staging slots.
-    constexpr int64_t LDS_BUDGET = 64 * 1024;
+    constexpr int64_t LDS_BUDGET = LDSKB * 1024;
     constexpr int64_t MFMA_PER_STAGE = 512;
     const int64_t mfma_per_ch = df * df * (NB / 4) * MW * NW;
     int64_t cc = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
@@ -563,12 +563,19 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 //  tiny    4 (k = 2) or 2 (k = 3) channels by 32 positions, the K loop split
 //          over 4 waves: small problems, spread over as many CUs as possible
 #ifndef CLIFF_W2
-#define CLIFF_W2 4, 1, 4, 8, 6, 2  // WCO, WPOS, MW, NW, SLOTS, waves/SIMD (k = 2)
+#define CLIFF_W2 4, 1, 4, 8, 6, 2, 1, 80  // WCO, WPOS, MW, NW, SLOTS, waves/SIMD, K split,
+                                         // LDS budget (KB, two stage buffers) (k = 2)
 #endif
 #ifndef CLIFF_W3
 #define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
 #endif
-#define CLIFF_W2_32 2, 2, 4, 8, 6, 2  // k = 2 wide variant for C_out <= 32
+#define CLIFF_W2_32 2, 2, 4, 8, 10, 2, 1, 80 // k = 2 wide variant for C_out <= 32
+// the 64-channel tile with 10 staging slots, for stages that need them
+// (large images or filters; 6 slots measured 0.4 % faster where they suffice)
+#define CLIFF_W2_S10 4, 1, 4, 8, 10, 2, 1, 80
+// the d_filter = 1 (linear) wide kernels keep 6 slots: with 9 they spill
+#define CLIFF_W2_LIN 4, 1, 4, 8, 6, 2, 1, 80
+#define CLIFF_W2_32_LIN 2, 2, 4, 8, 6, 2, 1, 80
 #define CLIFF_W3_32 4, 1, 4, 8, 6, 2  // k = 3, 3x3x3 wide variant for 16 < C_out <= 32
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
@@ -582,7 +589,8 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #define CLIFF_TINY2 1, 1, 1, 2, 12, 4, CLIFF_TINY_WK
 #define CLIFF_TINY3 1, 1, 1, 2, 12, 3, CLIFF_TINY_WK
 
-template <int NB, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES, int WK = 1>
+template <int NB, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES, int WK = 1,
+          int LDSKB = 64>
 struct Shape {
     static constexpr int co_wg = WCO * MW * (16 / NB);
     static constexpr int pos = WPOS * NW * 16;
@@ -593,14 +601,14 @@ struct Shape {
 };
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS, int WAVES,
-          int WK>
+          int WK, int LDSKB>
 cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream,
-                           Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>)
+                           Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB>)
 {
-    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>(p, stream);
+    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB>(p, stream);
 }
 
-template <int KD, int NB, int DF, class Wide>
+template <int KD, int NB, int DF, class Wide, class... WideAlt>
 cliff_status run_shapes(const ConvProblem& p, hipStream_t stream);
 
 template <int KD, int NB, int DF>
@@ -608,9 +616,16 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
 {
     // k = 2 has two wide tiles: 64 channels x 128 positions, and for
     // C_out <= 32 a 32 x 256 one, so the channels are not half wasted
-    if constexpr (KD == 2) {
+    if constexpr (KD == 2 && DF == 1) {
+        if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32_LIN>>(p, stream);
+        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_LIN>>(p, stream);
+    } else if constexpr (KD == 2) {
         if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32>>(p, stream);
-        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2>>(p, stream);
+        // 64 channels; when their stage needs more slots (large filters or
+        // images), the same tile with 10 slots, then the 32-channel tile,
+        // before the narrower shapes
+        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2>, Shape<NB, CLIFF_W2_S10>,
+                          Shape<NB, CLIFF_W2_32>>(p, stream);
     } else {
         // k = 3 with 3x3x3 filters and 17..32 output channels: all of them
         // in one 32 x 128 tile (measured +0.9 % at C = 32 against two 16 x
@@ -622,7 +637,7 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
     }
 }
 
-template <int KD, int NB, int DF, class Wide>
+template <int KD, int NB, int DF, class Wide, class... WideAlt>
 cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
 {
     using Medium = std::conditional_t<KD == 2, Shape<NB, CLIFF_MEDIUM2>, Shape<NB, CLIFF_MEDIUM3>>;
@@ -670,6 +685,11 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
         const bool forced = p.mfma_shape >= 0;
         cliff_status s = CLIFF_EUNSUPPORTED;
         if (o == 0 && (wide_ok || forced)) s = run_shape_cfg<KD, NB, DF, WCC>(p, stream, Wide{});
+        if (o == 0)
+            ((s = s == CLIFF_EUNSUPPORTED && (p.C_out * 2 > WideAlt::co_wg || forced)
+                      ? run_shape_cfg<KD, NB, DF, WCC>(p, stream, WideAlt{})
+                      : s),
+             ...);
         if (o == 1 && (medium_ok || forced)) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Medium{});
         if (o == 2) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Narrow{});
         if (o == 3) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Tiny{});

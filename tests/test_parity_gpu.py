@@ -315,3 +315,20 @@ def test_linear_parity(g, B, C_in, C_out):
     torch.cuda.synchronize()
     assert_parity(y.cpu().numpy(), oracle.act(ref[:, :, None, :], AGG_LINEAR, tuple(range(nb)),
                                               aw, ab)[:, :, 0, :])
+
+
+# 2D stages the 64-channel wide tile cannot hold in its 6 staging slots: wide
+# images and larger filters take the 10-slot tile or the 32-channel one.  With
+# the wide shape forced, the first two reach the 10-slot tile and the third
+# the 32-channel tile through both fallbacks (the automatic choice picks
+# smaller shapes for these small batches); full parity for both.
+WIDE_STAGE = [(1, 3, 40, 200, 3), (1, 2, 64, 60, 5), (1, 2, 48, 120, 5)]
+
+
+@pytest.mark.parametrize("shape", WIDE_STAGE, ids=str)
+def test_wide_tile_fallbacks(shape):
+    g = (1, 1)
+    s, x, f, b = _case(130 + shape[3], g, shape)
+    ref = oracle.conv_nd(x, f, b, g)
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
+        assert_parity(gpu_conv(g, x, f, b, algo=algo), ref, what="algo %d" % algo)
