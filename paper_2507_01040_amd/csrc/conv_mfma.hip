@@ -35,6 +35,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <cmath>
 #include <type_traits>
 
 #include "common.hpp"
@@ -44,6 +45,9 @@
 #define CLIFF_SGB_IL 2
 #endif
 
+#ifndef CLIFF_SHAPE_MODEL  // quantisation model for the tile choice of large problems
+#define CLIFF_SHAPE_MODEL 1
+#endif
 namespace cliff {
 namespace {
 
@@ -668,6 +672,35 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
         first = 1;
     else
         first = 3;
+    // Convolutions of >= 1 GFLOP: a quantisation model instead, fitted to
+    // timing every shape forced on 24 2D/3D problems (MI355X).  One block of
+    // any shape keeps its CU's matrix cores busy, so a shape's N blocks take
+    // ceil(N / CUs) rounds of whole blocks, and its rate is roughly
+    //     b * N / (ceil(N / CUs) * CUs) * C_out / (its channel blocks * CO_WG)
+    // with b its rate on large problems (fraction of the peak): wide 0.87
+    // (2D) / 0.90 (3D), medium 0.74 / 0.81, narrow 0.74, tiny 0.25.  The largest
+    // estimate goes first.  Smaller problems are latency-bound (the tiny
+    // tile's split K loop wins there) and keep the rule above; linear layers
+    // (d_filter = 1) too.
+    const double useful = 2.0 * M * p.C_out * NB * p.C_in * NB *
+                          std::pow((double)p.d_filter, KD);
+    const int cus = device_cus();
+    if (CLIFF_SHAPE_MODEL && p.d_filter > 1 && useful >= 1e9 && cus > 0) {
+        auto est = [&](bool ok, int64_t n, int co_wg, double b) {
+            if (!ok || n < 1) return 0.0;
+            const int64_t rounds = (n + cus - 1) / cus;
+            const double u =
+                (double)p.C_out / (double)(((p.C_out + co_wg - 1) / co_wg) * co_wg);
+            return b * (double)n / (double)(rounds * cus) * u;
+        };
+        const double e[4] = {est(wide_ok, bw, Wide::co_wg, KD == 2 ? 0.87 : 0.90),
+                             est(medium_ok, bm, Medium::co_wg, KD == 2 ? 0.74 : 0.81),
+                             est(true, bn, Narrow::co_wg, 0.74),
+                             est(true, Tiny::blocks(p, M), Tiny::co_wg, 0.25)};
+        first = 0;
+        for (int i = 1; i < 4; ++i)
+            if (e[i] > e[first]) first = i;
+    }
     int order[4] = {first, 0, 2, 1};
     int n_order = 4;
     if (p.mfma_shape >= 0) {
