@@ -39,6 +39,9 @@
 #ifndef CLIFF_W1  // wide tile: WCO, WPOS, MW, NW, input slots
 #define CLIFF_W1 2, 2, 4, 4, 8
 #endif
+#ifndef CLIFF_SHAPE_MODEL1  // quantisation model for the tile choice of large layers
+#define CLIFF_SHAPE_MODEL1 1
+#endif
 #ifndef CLIFF_X16  // 16-byte input staging when d_image and C_out are even
 #define CLIFF_X16 1
 #endif
@@ -514,6 +517,30 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     auto blocks = [&](int64_t co_wg, int64_t pos) {
         return ((M + pos - 1) / pos) * ((p.C_out + co_wg - 1) / co_wg);
     };
+    // Layers of >= 1 GFLOP: the quantisation model of the 2D/3D kernel (a
+    // shape's N blocks take ceil(N / CUs) rounds of whole blocks; rate
+    // b * N / (rounds * CUs) * channel utilisation), fitted to forced-shape
+    // timings of 10 1-D layers on MI355X: b = 0.90 (wide), 0.80 (narrow),
+    // 0.68 (tiny).  Smaller layers keep the latency rule below.
+    const double useful = 2.0 * M * p.C_out * 2 * p.C_in * 2 * p.d_filter;
+    const int cus = device_cus();
+    if (CLIFF_SHAPE_MODEL1 && useful >= 1e9 && cus > 0) {
+        auto est = [&](int64_t co_wg, int64_t pos, double b) {
+            const int64_t n = blocks(co_wg, pos);
+            const int64_t rounds = (n + cus - 1) / cus;
+            const double u =
+                (double)p.C_out / (double)(((p.C_out + co_wg - 1) / co_wg) * co_wg);
+            return b * (double)n / (double)(rounds * cus) * u;
+        };
+        const double ew = p.C_out > 32 ? est(64, 128, 0.90) : 0.0;
+        const double en = est(8, 256, 0.80), et = est(8, 32, 0.68);
+        cliff_status s = CLIFF_EUNSUPPORTED;
+        if (ew >= en && ew >= et) s = wide();
+        if (s == CLIFF_EUNSUPPORTED && en >= et) s = narrow();
+        if (s == CLIFF_EUNSUPPORTED) s = tiny();
+        if (s == CLIFF_EUNSUPPORTED) s = narrow();
+        return s;
+    }
     cliff_status s = CLIFF_EUNSUPPORTED;
     if (p.C_out > 32 && blocks(64, 128) >= 256) s = wide();
     if (s == CLIFF_EUNSUPPORTED) s = tiny();
