@@ -55,6 +55,7 @@ struct ConvProblem {
     SignMasks sign;
     ActParams act;
     int mfma_shape;  // -1: chosen from the problem; 0..3: wide, medium, narrow, tiny
+    int rowblk = 0;  // 2D: row-aligned blocks allowed (second pass, wide images)
 };
 
 // Two-layer block (conv + bias + act, twice) for the fused small-block kernel.

@@ -45,6 +45,9 @@
 #define CLIFF_SGB_IL 2
 #endif
 
+#ifndef CLIFF_ROWBLK  // 2D row-aligned blocks: 1 when no shape fits whole-row slabs, 2 always
+#define CLIFF_ROWBLK 1
+#endif
 #ifndef CLIFF_SHAPE_MODEL  // quantisation model for the tile choice of large problems
 #define CLIFF_SHAPE_MODEL 1
 #endif
@@ -64,6 +67,9 @@ struct MfmaArgs {
     int cc;         // input channels per stage
     int n_stage;    // ceil(C_in / cc) (k = 2) or that times d_filter (k = 3)
     int n_co_blk, n_blk;
+    int rowblk;     // 2D row-aligned blocks with column-window slabs (wide images)
+    int nseg;       // row-aligned blocks: blocks per output row
+    int sw;         // row-aligned blocks: slab row width in positions
     int stage_floats;  // LDS floats of one stage buffer
     SignMasks sign;
     ActParams act;
@@ -90,8 +96,13 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     const int taps2 = df * df;
     const int taps_full = KD == 2 ? taps2 : taps2 * df;
     const int D = a.D, Do = a.Do;
-    const int row_floats = D * NB;
-    const int row_f4 = row_floats / 4;
+    const int row_floats = D * NB;  // global row stride
+    // Row-aligned blocks (2D images too wide for whole-row slabs): a block is
+    // at most P positions of one output row, and its slab holds only the
+    // d_filter rows x (P + d_filter - 1) columns it reads.
+    const bool rb = KD == 2 && a.rowblk;
+    const int lrow_floats = rb ? a.sw * NB : row_floats;  // LDS slab row
+    const int lrow_f4 = lrow_floats / 4;
     const int tid = threadIdx.x;
 
     // Workgroups are dispatched round-robin over the 8 XCDs; renumber them so
@@ -105,8 +116,16 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     const int co_blk = tile % a.n_co_blk;
     const int pos_blk = tile / a.n_co_blk;
     const int co0 = co_blk * CO_WG;
-    const int m0 = pos_blk * P;
-    const int m_end = min(m0 + P, a.M);
+    int m0, m_end, x0 = 0;  // x0: first slab column (row-aligned blocks)
+    if (rb) {
+        const int seg = pos_blk % a.nseg, ry = pos_blk / a.nseg;  // output row over (b, y)
+        x0 = seg * P;
+        m0 = ry * Do + x0;
+        m_end = m0 + min(P, Do - x0);
+    } else {
+        m0 = pos_blk * P;
+        m_end = min(m0 + P, a.M);
+    }
 
     // Slab geometry: output rows r0..r1 (rows of d_out positions), planes
     // pl0..pl1 (2D: batch entry; 3D: (batch, z)).  Each plane contributes its
@@ -131,7 +150,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     // stage with nv < cc valid channels loads f < nv * slab_f4 (slab) and
     // f - cc * slab_f4 < nv * wch_f4 (filters).
     const int cc = CCT > 0 ? CCT : a.cc;  // CCT > 0: channels per stage fixed
-    const int slab_f4 = n_rows * row_f4;  // one channel's slab
+    const int slab_f4 = n_rows * lrow_f4;  // one channel's slab
     const int wq_f4 = taps2 * NB / 4;
     const int wch_f4 = CO_WG * wq_f4;     // one channel's filters
     const int total_f4 = cc * (slab_f4 + wch_f4);
@@ -149,11 +168,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         if (f < cc * slab_f4) {
             const int c_l = f / slab_f4;
             const int fr = f - c_l * slab_f4;
-            const int row = fr / row_f4;
-            const int sr = fr - row * row_f4;
+            const int row = fr / lrow_f4;
+            const int sr = fr - row * lrow_f4;
             // N_B = 8 rows are stored [half][x][4]: slot sr = half * D + x
-            // holds the global float4 2 x + half of the row
-            const int col = NB == 8 ? 2 * (sr % D) + sr / D : sr;
+            // holds the global float4 2 x + half of the row; row-aligned
+            // blocks stage columns x0 .. x0 + sw - 1
+            const int col = NB == 8 ? 2 * (sr % D) + sr / D : (rb ? min(x0 + sr, D - 1) : sr);
             int pl, yin;
             if (row < len0) {
                 pl = pl0;
@@ -253,7 +273,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         const int pl = r / Do;
         const int yy = r - pl * Do;
         const int srow = pl == pl0 ? yy - ylo0 : len0 + (pl - pl0 - 1) * D + yy;
-        xoff[nw] = srow * row_floats + xx * 4 + kk;
+        xoff[nw] = srow * lrow_floats + (xx - x0) * 4 + kk;
     }
 
     f4 acc[MW][NW];
@@ -295,7 +315,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
             for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[wofs[h] + mw * wtile + tap * NB];
 #pragma unroll
             for (int nw = 0; nw < NW; ++nw)
-                Bv[nw] = S[xoff[nw] + qy * row_floats + h * D * 4 + qx * 4];
+                Bv[nw] = S[xoff[nw] + qy * lrow_floats + h * D * 4 + qx * 4];
         };
         auto chan = [&](int c, auto base_c) {
             constexpr int BASE = decltype(base_c)::value;  // buffer of step 0
@@ -378,7 +398,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
                                 av[mw] = Sw[wofs[h] + mw * wtile + tap * NB] * sg[h];
 #pragma unroll
                             for (int nw = 0; nw < NW; ++nw)
-                                bv[nw] = S[xoff[nw] + qy_ * row_floats + h * D * 4 +
+                                bv[nw] = S[xoff[nw] + qy_ * lrow_floats + h * D * 4 +
                                            qx_ * 4];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
@@ -490,28 +510,49 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     int64_t npos = 1;
     for (int t = 0; t < KD; ++t) npos *= Do;
     const int64_t M = p.B * npos;
-    const int64_t n_pos_blk = (M + P - 1) / P;
+    int64_t n_pos_blk = (M + P - 1) / P;
     const int64_t n_co_blk = (p.C_out + CO_WG - 1) / CO_WG;
-    const int64_t n_blk = n_pos_blk * n_co_blk;
-    if (M >= (1ll << 31) || n_blk >= (1ll << 31) || D * D * NB >= (1 << 24))
-        return CLIFF_EUNSUPPORTED;
+    if (M >= (1ll << 31) || D * D * NB >= (1 << 24)) return CLIFF_EUNSUPPORTED;
     // Upper bound of the slab rows of any block.
     const int64_t total_rows = M / Do;
     const int64_t R = std::min<int64_t>((P - 1) / Do + 2, total_rows);
     const int64_t planes = std::min<int64_t>(R, (R - 1) / Do + 2);
     const int64_t rows_max = R + planes * (df - 1);
-    const int64_t ch_floats = rows_max * D * NB + CO_WG * df * df * NB;  // per channel
+    int64_t ch_floats = rows_max * D * NB + CO_WG * df * df * NB;  // per channel
     // Channels per stage: enough MFMAs per wave between barriers, within the
     // LDS budget (two buffers) and the staging slots.
     constexpr int64_t LDS_BUDGET = LDSKB * 1024;
     constexpr int64_t MFMA_PER_STAGE = 512;
     const int64_t mfma_per_ch = df * df * (NB / 4) * MW * NW;
-    int64_t cc = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
-    cc = std::min<int64_t>(cc, LDS_BUDGET / (2 * ch_floats * 4));
-    cc = std::min<int64_t>(cc, (int64_t)SLOTS * NT / (ch_floats / 4));
-    if (CCT > 0) cc = cc >= CCT ? CCT : 0;
-    if (WK > 1 && cc > WK) cc -= cc % WK;  // equal channel shares for the K slices
+    auto channels = [&](int64_t chf) {
+        int64_t c = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
+        c = std::min<int64_t>(c, LDS_BUDGET / (2 * chf * 4));
+        c = std::min<int64_t>(c, (int64_t)SLOTS * NT / (chf / 4));
+        if (CCT > 0) c = c >= CCT ? CCT : 0;
+        if (WK > 1 && c > WK) c -= c % WK;  // equal channel shares for the K slices
+        return c;
+    };
+    int64_t cc = channels(ch_floats);
+    // 2D images whose whole-row slabs do not fit: row-aligned blocks with
+    // column-window slabs (d_filter rows of min(P, d_out) + d_filter - 1
+    // positions)
+    int rowblk = 0;
+    int64_t nseg = 1, sw = 0;
+    if (KD == 2 && (CLIFF_ROWBLK == 2 || (cc < 1 && CLIFF_ROWBLK == 1 && p.rowblk))) {
+        sw = std::min<int64_t>(P, Do) + df - 1;
+        const int64_t chf = df * sw * NB + CO_WG * df * df * NB;
+        const int64_t c = channels(chf);
+        if (c >= 1) {
+            ch_floats = chf;
+            cc = c;
+            nseg = (Do + P - 1) / P;
+            n_pos_blk = p.B * Do * nseg;
+            rowblk = 1;
+        }
+    }
     if (cc < 1) return CLIFF_EUNSUPPORTED;
+    const int64_t n_blk = n_pos_blk * n_co_blk;
+    if (n_blk >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
     const int64_t stage_floats = cc * ch_floats;
     // the K split's partial sums reuse the stage buffers after the loop
     const int64_t red_bytes = (int64_t)(WK - 1) * WCO * WPOS * MW * NW * 64 * 16;
@@ -541,6 +582,9 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     a.n_stage = (int)(KD == 2 ? n_cgrp : n_cgrp * df);
     a.n_co_blk = (int)n_co_blk;
     a.n_blk = (int)n_blk;
+    a.rowblk = rowblk;
+    a.nseg = (int)nseg;
+    a.sw = (int)sw;
     a.stage_floats = (int)stage_floats;
     a.sign = p.sign;
     a.act = p.act;
@@ -548,9 +592,9 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
         fprintf(stderr,
                 "cliffconv: conv_mfma k=%d d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
                 "(%d channels x %d positions), K split over %d waves, %lld workgroups, "
-                "%d channels/stage, %lld LDS bytes\n",
+                "%d channels/stage, %lld LDS bytes%s\n",
                 KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, WK, (long long)n_blk, (int)cc,
-                (long long)lds_bytes);
+                (long long)lds_bytes, rowblk ? ", row-aligned blocks" : "");
     hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
@@ -712,25 +756,38 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
     // register use down); the other shapes choose the channels per stage at
     // run time
     constexpr int WCC = DF == 3 ? 1 : 0;
-    for (int i = 0; i < n_order; ++i) {
-        const int o = order[i];
-        if (i > 0 && o == order[0]) continue;
-        const bool forced = p.mfma_shape >= 0;
-        cliff_status s = CLIFF_EUNSUPPORTED;
-        if (o == 0 && (wide_ok || forced)) s = run_shape_cfg<KD, NB, DF, WCC>(p, stream, Wide{});
-        if (o == 0)
-            ((s = s == CLIFF_EUNSUPPORTED && (p.C_out * 2 > WideAlt::co_wg || forced)
-                      ? run_shape_cfg<KD, NB, DF, WCC>(p, stream, WideAlt{})
-                      : s),
-             ...);
-        if (o == 1 && (medium_ok || forced)) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Medium{});
-        if (o == 2) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Narrow{});
-        if (o == 3) s = run_shape_cfg<KD, NB, DF, 0>(p, stream, Tiny{});
-        if (s != CLIFF_EUNSUPPORTED) return s;
+    auto attempt = [&](const ConvProblem& q) {
+        for (int i = 0; i < n_order; ++i) {
+            const int o = order[i];
+            if (i > 0 && o == order[0]) continue;
+            const bool forced = q.mfma_shape >= 0;
+            cliff_status s = CLIFF_EUNSUPPORTED;
+            if (o == 0 && (wide_ok || forced))
+                s = run_shape_cfg<KD, NB, DF, WCC>(q, stream, Wide{});
+            if (o == 0)
+                ((s = s == CLIFF_EUNSUPPORTED && (q.C_out * 2 > WideAlt::co_wg || forced)
+                          ? run_shape_cfg<KD, NB, DF, WCC>(q, stream, WideAlt{})
+                          : s),
+                 ...);
+            if (o == 1 && (medium_ok || forced))
+                s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Medium{});
+            if (o == 2) s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Narrow{});
+            if (o == 3) s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Tiny{});
+            if (s != CLIFF_EUNSUPPORTED) return s;
+        }
+        if (q.mfma_shape < 0 && first != 3)
+            return run_shape_cfg<KD, NB, DF, 0>(q, stream, Tiny{});
+        return CLIFF_EUNSUPPORTED;
+    };
+    // whole-row slabs first (flattened blocks waste no positions); 2D images
+    // too wide for them in every shape then take row-aligned blocks
+    cliff_status s = attempt(p);
+    if (s == CLIFF_EUNSUPPORTED && KD == 2 && CLIFF_ROWBLK == 1) {
+        ConvProblem q = p;
+        q.rowblk = 1;
+        s = attempt(q);
     }
-    if (p.mfma_shape < 0 && first != 3)
-        return run_shape_cfg<KD, NB, DF, 0>(p, stream, Tiny{});
-    return CLIFF_EUNSUPPORTED;
+    return s;
 }
 
 }  // namespace

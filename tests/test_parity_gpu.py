@@ -332,3 +332,31 @@ def test_wide_tile_fallbacks(shape):
     ref = oracle.conv_nd(x, f, b, g)
     for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
         assert_parity(gpu_conv(g, x, f, b, algo=algo), ref, what="algo %d" % algo)
+
+
+# 2D images too wide for whole-row slabs in every tile shape (600 and 520
+# positions, 3x3 and 5x5 filters): row-aligned blocks with column-window
+# slabs; each tile shape forced, outputs sampled (every row end, both
+# channel ends, random positions) against the oracle computed point by point
+ROW_BLOCKS = [(1, 3, 40, 600, 3), (2, 2, 64, 520, 5), (1, 2, 8, 1030, 3)]
+
+
+@pytest.mark.parametrize("shape", ROW_BLOCKS, ids=str)
+def test_row_aligned_blocks(shape):
+    g = (1, 1)
+    B, C_in, C_out, D, df = shape
+    s, x, f, b = _case(150 + D, g, shape)
+    Do = D - df + 1
+    rng = np.random.default_rng(D)
+    pts = [(bb, co, y * Do + xx) for bb in range(B) for co in (0, C_out - 1)
+           for y in (0, Do - 1) for xx in (0, 127, 128, Do - 1)]
+    pts += [(int(rng.integers(B)), int(rng.integers(C_out)), int(rng.integers(Do * Do)))
+            for _ in range(600)]
+    bs = np.array([p[0] for p in pts])
+    cos = np.array([p[1] for p in pts])
+    flat = np.array([p[2] for p in pts])
+    ref = oracle.conv_points(x, f, b, g, bs, cos, flat)
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        got = y.reshape(B, C_out, Do * Do, 4)[bs, cos, flat]
+        assert_parity(got, ref, what="algo %d" % algo)
