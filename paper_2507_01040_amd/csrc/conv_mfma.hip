@@ -45,6 +45,10 @@
 #define CLIFF_SGB_IL 2
 #endif
 
+#ifndef CLIFF_PRO_SB  // scheduling barrier after a channel's prologue reads
+#define CLIFF_PRO_SB 1
+#endif
+
 #ifndef CLIFF_ROWBLK  // 2D row-aligned blocks: 1 when no shape fits whole-row slabs, 2 always
 #define CLIFF_ROWBLK 1
 #endif
@@ -358,6 +362,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #pragma unroll
             for (int u = 0; u < PF; ++u)
                 if (u < T) ld(c, u, fa[u], fb[u]);
+#if CLIFF_PRO_SB
+            // issue the prologue's reads together, ahead of the first step
+            // (else they are spread between the first step's own MFMAs, each
+            // of which then waits for its read)
+            __builtin_amdgcn_sched_barrier(0);
+#endif
         };
         if constexpr (CCT == 1) {
             prologue(0);
