@@ -543,12 +543,18 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
         return c;
     };
     int64_t cc = channels(ch_floats);
-    // 2D images whose whole-row slabs do not fit: row-aligned blocks with
-    // column-window slabs (d_filter rows of min(P, d_out) + d_filter - 1
-    // positions)
+    // Row-aligned blocks with column-window slabs (d_filter rows of
+    // min(P, d_out) + d_filter - 1 positions): for 2D images whose whole-row
+    // slabs do not fit, and on the wide tiles wherever a row's blocks leave
+    // at most 2 % of their positions idle (d_out just under a multiple of
+    // P): their slabs are 3 rows instead of up to 7, measured +0.1-0.9 % on
+    // such images (d_out = 126, 254, 256, 382, 638) and far slower elsewhere.
+    const int64_t nseg_r = (Do + P - 1) / P;
+    const bool snug = MW * NW >= 32 && Do * 50 >= nseg_r * P * 49;
     int rowblk = 0;
     int64_t nseg = 1, sw = 0;
-    if (KD == 2 && (CLIFF_ROWBLK == 2 || (cc < 1 && CLIFF_ROWBLK == 1 && p.rowblk))) {
+    if (KD == 2 && (CLIFF_ROWBLK == 2 || (p.rowblk == 2 && snug) ||
+                    (cc < 1 && CLIFF_ROWBLK == 1 && p.rowblk == 1))) {
         sw = std::min<int64_t>(P, Do) + df - 1;
         const int64_t chf = df * sw * NB + CO_WG * df * df * NB;
         const int64_t c = channels(chf);
@@ -789,9 +795,13 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
             return run_shape_cfg<KD, NB, DF, 0>(q, stream, Tiny{});
         return CLIFF_EUNSUPPORTED;
     };
-    // whole-row slabs first (flattened blocks waste no positions); 2D images
-    // too wide for them in every shape then take row-aligned blocks
-    cliff_status s = attempt(p);
+    // whole-row slabs first (flattened blocks waste no positions) except on
+    // the wide tiles where row-aligned blocks leave almost none idle (rowblk
+    // 2); 2D images too wide for whole-row slabs in every shape then take
+    // row-aligned blocks
+    ConvProblem p0 = p;
+    if (KD == 2 && CLIFF_ROWBLK == 1 && p0.rowblk == 0) p0.rowblk = 2;
+    cliff_status s = attempt(p0);
     if (s == CLIFF_EUNSUPPORTED && KD == 2 && CLIFF_ROWBLK == 1) {
         ConvProblem q = p;
         q.rowblk = 1;
