@@ -360,3 +360,46 @@ def test_row_aligned_blocks(shape):
         y = gpu_conv(g, x, f, b, algo=algo)
         got = y.reshape(B, C_out, Do * Do, 4)[bs, cos, flat]
         assert_parity(got, ref, what="algo %d" % algo)
+
+
+# Images whose d_out is just under (or at) a multiple of the wide tiles'
+# P positions (128 for the 64-channel tile, 256 for the 32-channel one):
+# those tiles take row-aligned blocks there (at most 2 % of a block row
+# idle).  Odd input channel counts, a non-trivial signature, the fused
+# activation on one case; outputs sampled (every row end, both channel ends,
+# random positions) against the oracle computed point by point.
+SNUG = [(2, 5, 64, 130, 3, (1, -1), None),       # d_out 128 = P
+        (1, 3, 70, 128, 3, (-1, -1), "mean"),    # d_out 126, two channel blocks
+        (1, 3, 32, 258, 3, (1, 1), None),        # 32-channel tile, d_out 256 = P
+        (1, 7, 64, 256, 3, (0, 1), "linear")]    # d_out 254 = 2 P - 2
+
+
+@pytest.mark.parametrize("case", SNUG, ids=str)
+def test_snug_row_aligned_blocks(case):
+    B, C_in, C_out, D, df, g, mode = case
+    s, x, f, b = _case(170 + D + C_in, g, (B, C_in, C_out, D, df))
+    Do = D - df + 1
+    rng = np.random.default_rng(D + C_out)
+    act = None
+    if mode is not None:
+        blades = (0, 1, 2, 3)
+        aw = rng.standard_normal((C_out, 4)).astype(np.float32) if mode == "linear" else None
+        ab = rng.standard_normal(C_out).astype(np.float32) if mode == "linear" else None
+        act = (AGG_LINEAR if mode == "linear" else AGG_MEAN, blades, aw, ab)
+    pts = [(bb, co, y * Do + xx) for bb in range(B) for co in (0, C_out - 1)
+           for y in (0, Do // 2, Do - 1) for xx in (0, 1, 127, 128, Do - 2, Do - 1) if xx < Do]
+    pts += [(int(rng.integers(B)), int(rng.integers(C_out)), int(rng.integers(Do * Do)))
+            for _ in range(800)]
+    bs = np.array([p[0] for p in pts])
+    cos = np.array([p[1] for p in pts])
+    flat = np.array([p[2] for p in pts])
+    ref = oracle.conv_points(x, f, b, g, bs, cos, flat)
+    if act is not None:
+        # each sampled point as its own channel, with its channel's gate
+        ref = oracle.act(ref[None], act[0], act[1],
+                         None if act[2] is None else act[2][cos],
+                         None if act[3] is None else act[3][cos])[0]
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
+        y = gpu_conv(g, x, f, b, act=act, algo=algo)
+        got = y.reshape(B, C_out, Do * Do, 4)[bs, cos, flat]
+        assert_parity(got, ref, what="algo %d" % algo)
