@@ -21,7 +21,10 @@
 // Work decomposition.  The flattened output positions m in [0, B d_out^k)
 // are cut into blocks of P consecutive positions (they may span rows, planes
 // and batch entries); a workgroup computes P positions x CO_WG output
-// channels.  The K loop runs over "stages": cc input channels (2D) or cc
+// channels.  2D images may instead use row-aligned blocks (at most P
+// positions of one output row, staging only the d_filter input rows and the
+// columns they read): where whole-row slabs do not fit, and on the wide
+// tiles where a row's blocks leave at most 2 % of their positions idle.  The K loop runs over "stages": cc input channels (2D) or cc
 // input channels of one filter plane qz (3D); the host picks cc so a stage
 // holds enough MFMAs per barrier.  For each stage and channel the workgroup
 // stages in LDS (double-buffered, direct global->LDS loads):

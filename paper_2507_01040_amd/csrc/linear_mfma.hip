@@ -8,7 +8,9 @@
 // are small (the paper's linear layers have 32 channels), so:
 //  * every workgroup copies the raw weight [C_in, C_out, N_B] into LDS once;
 //    A fragments are read from there and the sign applied in a register, so
-//    the expanded weight exists nowhere;
+//    the expanded weight exists nowhere (layers of 128 or 256 columns without
+//    zero signs also keep the negated weight, and each lane reads the copy
+//    of its sign instead of multiplying);
 //  * each wave owns whole rows of Y (a tile of 16 * NWW positions by all N
 //    columns) and streams its tiles without any barrier: B fragments come from
 //    HBM straight into registers, PF chunks of 16 K values ahead, across tile
