@@ -68,14 +68,19 @@ struct LinArgs {
 #ifndef CLIFF_LIN_NEG  // negated weight copy in LDS instead of sign multiplies
 #define CLIFF_LIN_NEG 1
 #endif
+#ifndef CLIFF_LIN_NEG8  // 8-wave workgroups for 256-column layers whose two copies need them
+#define CLIFF_LIN_NEG8 1
+#endif
 #ifndef CLIFF_LIN_WAVES  // waves per SIMD the registers are sized for
 #define CLIFF_LIN_WAVES 2
 #endif
 
 // NEG: LDS holds the weight and its negation; each lane's A reads take the
 // copy of its sign, so no step multiplies (signatures without zero signs).
-template <int NB, int RT, int KQ, int NWW, int PF, int WAVES, bool NEG>
-__global__ __launch_bounds__(256, WAVES) void linear_mfma_kernel(LinArgs a)
+// NT threads per workgroup (4 waves; 8 where one workgroup per CU holds
+// both weight copies).
+template <int NB, int RT, int KQ, int NWW, int PF, int WAVES, bool NEG, int NT = 256>
+__global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
 {
     static_assert(KQ % PF == 0 && KQ >= PF, "whole prefetch rounds per tile");
     constexpr int N = 16 * RT;
@@ -278,16 +283,16 @@ __global__ __launch_bounds__(256, WAVES) void linear_mfma_kernel(LinArgs a)
 
 // Resident workgroups per CU of one kernel instantiation at an LDS size,
 // cached per instantiation (packed (lds << 8) | occ); 0 when the query fails.
-template <int NB, int RT, int KQ, int NWW, int PF, int WAVES, bool NEG>
+template <int NB, int RT, int KQ, int NWW, int PF, int WAVES, bool NEG, int NT = 256>
 int linear_occupancy(int64_t lds)
 {
     static std::atomic<int64_t> cache{0};
-    auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, NEG>;
+    auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, NEG, NT>;
     const int64_t c = cache.load(std::memory_order_relaxed);
     if ((c >> 8) == lds && (c & 0xff)) return (int)(c & 0xff);
     int occ = 0;
     if (lds > 160 * 1024 ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, 256, (size_t)lds) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, NT, (size_t)lds) != hipSuccess ||
         occ < 1)
         return 0;
     cache.store((lds << 8) | std::min(occ, 255), std::memory_order_relaxed);
@@ -326,12 +331,32 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     // (interleaved): 3D C = 32 (N = 256) +3.4 %, 1-D C = 64 (N = 128)
     // +1.7 %, the other N = 128 layers within noise; the HBM-bound N = 64
     // layer -2 %, so it keeps the multiplies.
-    const bool neg = CLIFF_LIN_NEG && RT >= 8 && p.sign.zero == 0 &&
+    const bool neg_ok = CLIFF_LIN_NEG && RT >= 8 && p.sign.zero == 0;
+    const bool neg = neg_ok &&
                      linear_occupancy<NB, RT, KQ, NWW, PF, WAVES, true>(2 * wbytes + tail) >= occ;
-    const int64_t lds = (neg ? 2 : 1) * wbytes + tail;
+    // 256-column layers whose weight copies leave room for only one 4-wave
+    // workgroup per CU: 8-wave workgroups share them at twice the waves per
+    // SIMD, with both copies where those fit at the 4-wave residency (64
+    // input channels in 2D), else with the weight alone where it holds a CU
+    // to one 4-wave workgroup (128 input channels in 1-D)
+    int occ8 = 0;
+    bool neg8 = false, plain8 = false;
+    if constexpr (RT == 16 && KQ == 16 && CLIFF_LIN_NEG8) {
+        if (neg_ok && !neg) {
+            occ8 = linear_occupancy<NB, RT, KQ, NWW, PF, WAVES, true, 512>(2 * wbytes + tail);
+            neg8 = occ8 > 0 && 2 * occ8 >= occ;
+        }
+        if (!neg && !neg8 && occ == 1) {
+            occ8 = linear_occupancy<NB, RT, KQ, NWW, PF, WAVES, false, 512>(wbytes + tail);
+            plain8 = occ8 >= 1;
+        }
+    }
+    const int64_t lds = (neg || neg8 ? 2 : 1) * wbytes + tail;
     const int cus = device_cus();
     if (cus < 1) return CLIFF_EDEVICE;
-    const int64_t n_wg = std::min<int64_t>((n_wt + 3) / 4, (int64_t)cus * occ);
+    const int wg_waves = neg8 || plain8 ? 8 : 4;
+    const int64_t n_wg = std::min<int64_t>((n_wt + wg_waves - 1) / wg_waves,
+                                           (int64_t)cus * (neg8 || plain8 ? occ8 : occ));
 
     LinArgs a;
     a.x = p.x;
@@ -347,9 +372,21 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     if (debug_enabled())
         fprintf(stderr,
                 "cliffconv: linear_mfma N_B=%d N=%d K=%d, %d positions per wave tile, "
-                "%lld wave tiles, %lld workgroups (%d per CU), %lld LDS bytes%s\n",
-                NB, N, 16 * KQ, TP, (long long)n_wt, (long long)n_wg, occ, (long long)lds,
-                neg ? ", negated weight copy" : "");
+                "%lld wave tiles, %lld workgroups of %d waves (%d per CU), %lld LDS bytes%s\n",
+                NB, N, 16 * KQ, TP, (long long)n_wt, (long long)n_wg, wg_waves,
+                neg8 || plain8 ? occ8 : occ, (long long)lds,
+                neg || neg8 ? ", negated weight copy" : "");
+    if constexpr (RT == 16 && KQ == 16 && CLIFF_LIN_NEG8) {
+        if (neg8 || plain8) {
+            if (neg8)
+                hipLaunchKernelGGL((linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, true, 512>),
+                                   dim3((unsigned)n_wg), dim3(512), (size_t)lds, stream, a);
+            else
+                hipLaunchKernelGGL((linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, false, 512>),
+                                   dim3((unsigned)n_wg), dim3(512), (size_t)lds, stream, a);
+            return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
+        }
+    }
     hipLaunchKernelGGL(neg ? kern_neg : kern, dim3((unsigned)n_wg), dim3(256), (size_t)lds,
                        stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
