@@ -190,6 +190,23 @@ def _stream_ptr(stream) -> int:
     return int(s.cuda_stream)
 
 
+def from_paper_protocol(filters, bias=None):
+    """Filters (N_B, C_in, C_out, d_f^k) and bias (N_B, C_out) in the paper's
+    input/output protocol ("Optimization Performed", convolutional layers:
+    blade axis first) to the library's blade-last layouts [C_in, C_out,
+    d_f^k, N_B] and [C_out, N_B], as contiguous copies (numpy arrays or torch
+    tensors, on the device they are on).  A caller-side layout conversion,
+    done once per set of weights; no step of the layer runs here."""
+    def last(a):
+        if a is None:
+            return None
+        if hasattr(a, "movedim"):
+            return a.movedim(0, -1).contiguous()
+        import numpy as np
+        return np.ascontiguousarray(np.moveaxis(a, 0, -1))
+    return last(filters), last(bias)
+
+
 def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
             out=None, stream=None, algo: int = ALGO_AUTO):
     """Clifford convolution of GPU tensors x [B,C_in,d^k,N_B] and filters
