@@ -376,7 +376,7 @@ def main():
                     help="only run N copies of 1 GiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the convolution would shard over the batch with no exchange); "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)

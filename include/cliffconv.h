@@ -51,7 +51,7 @@ typedef enum {
     CLIFF_ESHAPE = 2,       /* non-positive size, d_filter > d_image, overflow */
     CLIFF_EALIGN = 3,       /* tensor pointer not 16-byte aligned */
     CLIFF_EOVERLAP = 4,     /* output memory overlaps an input */
-    CLIFF_EUNSUPPORTED = 5, /* valid request this build cannot run */
+    CLIFF_EUNSUPPORTED = 5, /* valid request the library does not support */
     CLIFF_EDEVICE = 6       /* HIP reported an error */
 } cliff_status;
 

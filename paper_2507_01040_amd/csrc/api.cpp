@@ -416,7 +416,7 @@ const char* cliffconv_status_string(cliff_status s)
     case CLIFF_ESHAPE: return "invalid shape";
     case CLIFF_EALIGN: return "pointer not aligned";
     case CLIFF_EOVERLAP: return "output overlaps an input";
-    case CLIFF_EUNSUPPORTED: return "unsupported by this build";
+    case CLIFF_EUNSUPPORTED: return "unsupported by the library";
     case CLIFF_EDEVICE: return "HIP device error";
     }
     return "unknown status";
