@@ -644,6 +644,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #define CLIFF_W2_LIN 4, 1, 4, 8, 6, 2, 1, 80
 #define CLIFF_W2_32_LIN 2, 2, 4, 8, 6, 2, 1, 80
 #define CLIFF_W3_32 4, 1, 4, 8, 6, 2  // k = 3, 3x3x3 wide variant for 16 < C_out <= 32
+#define CLIFF_W3_32_96 4, 1, 4, 6, 6, 2  // the same with 96 positions (6 tiles per wave)
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
 #define CLIFF_NARROW 1, 4, 2, 4, 8, 2
@@ -698,8 +699,27 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
         // in one 32 x 128 tile (measured +0.9 % at C = 32 against two 16 x
         // 128 blocks; with 64 channels the 16 x 128 tile stays 2 % faster)
         if constexpr (DF == 3)
-            if (p.C_out <= 32 && p.C_out > 16)
-                return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3_32>>(p, stream);
+            if (p.C_out <= 32 && p.C_out > 16) {
+                // Two widths, 128 and 96 positions: on problems of >= 1 GFLOP
+                // the quantisation model (below) takes the one whose blocks
+                // fill the last round of CUs better.  Measured (interleaved):
+                // B = 8, d 32 -> 30 +2.8 % with 96, d 42 -> 40 +2.4 %; d 34
+                // -> 32 (2048 blocks of 128) -4 % with 96; d 24 -> 22, where
+                // only 96 makes the wide tile worth taking, +13 %.
+                using W128 = Shape<NB, CLIFF_W3_32>;
+                using W96 = Shape<NB, CLIFF_W3_32_96>;
+                int64_t M = p.B;
+                for (int t = 0; t < KD; ++t) M *= p.d_out;
+                const double useful = 2.0 * M * p.C_out * NB * p.C_in * NB * 27.0;
+                const int cus = device_cus();
+                auto fill = [&](int64_t n) {
+                    return (double)n / (double)(((n + cus - 1) / cus) * cus);
+                };
+                if (p.mfma_shape < 0 && useful >= 1e9 && cus > 0 &&
+                    fill(W96::blocks(p, M)) > fill(W128::blocks(p, M)))
+                    return run_shapes<KD, NB, DF, W96>(p, stream);
+                return run_shapes<KD, NB, DF, W128>(p, stream);
+            }
         return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3>>(p, stream);
     }
 }

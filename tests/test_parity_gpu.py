@@ -403,3 +403,29 @@ def test_snug_row_aligned_blocks(case):
         y = gpu_conv(g, x, f, b, act=act, algo=algo)
         got = y.reshape(B, C_out, Do * Do, 4)[bs, cos, flat]
         assert_parity(got, ref, what="algo %d" % algo)
+
+
+# 3D, 3x3x3 filters, 16 < C_out <= 32, >= 1 GFLOP: the automatic choice takes
+# the 32-channel wide tile at 96 positions per block where its blocks fill
+# the last round of CUs better than 128 (here 2250 blocks against 1688 on
+# 256 CUs: 9 rounds 98 % full against 7 rounds 94 % full); outputs sampled
+# (every batch entry, both channel ends, the corners of the output volume,
+# random positions) against the oracle point by point
+@pytest.mark.parametrize("g", [(1, 1, 1), (1, -1, 0)], ids=str)
+def test_3d_wide_96_positions(g):
+    B, C_in, C_out, D, df = 8, 4, 32, 32, 3
+    s, x, f, b = _case(190, g, (B, C_in, C_out, D, df))
+    Do = D - df + 1
+    rng = np.random.default_rng(191)
+    corners = [z * Do * Do + y * Do + xx for z in (0, Do - 1) for y in (0, Do - 1) for xx in (0, Do - 1)]
+    pts = [(bb, co, c) for bb in range(B) for co in (0, C_out - 1) for c in corners]
+    pts += [(int(rng.integers(B)), int(rng.integers(C_out)), int(rng.integers(Do ** 3)))
+            for _ in range(1500)]
+    bs = np.array([p[0] for p in pts])
+    cos = np.array([p[1] for p in pts])
+    flat = np.array([p[2] for p in pts])
+    ref = oracle.conv_points(x, f, b, g, bs, cos, flat)
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        got = y.reshape(B, C_out, Do ** 3, 8)[bs, cos, flat]
+        assert_parity(got, ref, what="algo %d" % algo)
