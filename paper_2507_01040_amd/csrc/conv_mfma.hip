@@ -52,6 +52,10 @@
 #define CLIFF_PRO_SB 1
 #endif
 
+#ifndef CLIFF_W2_WIDTH_MODEL  // 2D 64-channel tile: 128 or 96 positions by the quantisation model
+#define CLIFF_W2_WIDTH_MODEL 1
+#endif
+
 #ifndef CLIFF_ROWBLK  // 2D row-aligned blocks: 1 when no shape fits whole-row slabs, 2 always
 #define CLIFF_ROWBLK 1
 #endif
@@ -640,6 +644,8 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 // the 64-channel tile with 10 staging slots, for stages that need them
 // (large images or filters; 6 slots measured 0.4 % faster where they suffice)
 #define CLIFF_W2_S10 4, 1, 4, 8, 10, 2, 1, 80
+// the 64-channel tile 96 positions wide (4x6 tiles per wave)
+#define CLIFF_W2_96 4, 1, 4, 6, 6, 2, 1, 80
 // the d_filter = 1 (linear) wide kernels keep 6 slots: with 9 they spill
 #define CLIFF_W2_LIN 4, 1, 4, 8, 6, 2, 1, 80
 #define CLIFF_W2_32_LIN 2, 2, 4, 8, 6, 2, 1, 80
@@ -692,7 +698,27 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
         // 64 channels; when their stage needs more slots (large filters or
         // images), the same tile with 10 slots, then the 32-channel tile,
         // before the narrower shapes
-        return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2>, Shape<NB, CLIFF_W2_S10>,
+        // On problems of >= 1 GFLOP, 128 or 96 positions per block: the
+        // width whose blocks fill the last round of CUs better (the 128 tile's
+        // row-aligned blocks counted where they are snug, as the kernel takes
+        // them; the 96 tile, with 24 MFMA tiles per wave, never takes them)
+        using W128 = Shape<NB, CLIFF_W2>;
+        using W96 = Shape<NB, CLIFF_W2_96>;
+        const int64_t Do = p.d_out, M = p.B * Do * Do;
+        const double useful = 2.0 * M * p.C_out * NB * p.C_in * NB * (double)(p.d_filter * p.d_filter);
+        const int cus = device_cus();
+        auto nblk = [&](int64_t P, bool snug_ok) {
+            const int64_t nseg = (Do + P - 1) / P;
+            return snug_ok && Do * 50 >= nseg * P * 49 ? p.B * Do * nseg : (M + P - 1) / P;
+        };
+        auto fill = [&](int64_t n) {
+            return (double)n / (double)(((n + cus - 1) / cus) * cus);
+        };
+        if (CLIFF_W2_WIDTH_MODEL && p.mfma_shape < 0 && useful >= 1e9 && cus > 0 &&
+            fill(nblk(W96::pos, false)) > fill(nblk(W128::pos, true)))
+            return run_shapes<KD, NB, DF, W96, Shape<NB, CLIFF_W2_S10>, Shape<NB, CLIFF_W2_32>>(
+                p, stream);
+        return run_shapes<KD, NB, DF, W128, Shape<NB, CLIFF_W2_S10>,
                           Shape<NB, CLIFF_W2_32>>(p, stream);
     } else {
         // k = 3 with 3x3x3 filters and 17..32 output channels: all of them

@@ -429,3 +429,28 @@ def test_3d_wide_96_positions(g):
         y = gpu_conv(g, x, f, b, algo=algo)
         got = y.reshape(B, C_out, Do ** 3, 8)[bs, cos, flat]
         assert_parity(got, ref, what="algo %d" % algo)
+
+
+# 2D, >= 1 GFLOP, 64 output channels: the automatic choice takes the wide
+# tile at 96 positions per block where its blocks fill the last round of CUs
+# better than 128 (here 737 blocks, 96 % of 3 rounds on 256 CUs, against
+# 553, 72 %); sampled outputs (every batch entry, both channel ends, image
+# corners, random positions) against the oracle point by point
+@pytest.mark.parametrize("g", [(1, 1), (-1, 0)], ids=str)
+def test_2d_wide_96_positions(g):
+    B, C_in, C_out, D, df = 8, 4, 64, 96, 3
+    s, x, f, b = _case(200, g, (B, C_in, C_out, D, df))
+    Do = D - df + 1
+    rng = np.random.default_rng(201)
+    corners = [y * Do + xx for y in (0, 1, Do - 1) for xx in (0, Do // 2, Do - 1)]
+    pts = [(bb, co, c) for bb in range(B) for co in (0, C_out - 1) for c in corners]
+    pts += [(int(rng.integers(B)), int(rng.integers(C_out)), int(rng.integers(Do * Do)))
+            for _ in range(1500)]
+    bs = np.array([p[0] for p in pts])
+    cos = np.array([p[1] for p in pts])
+    flat = np.array([p[2] for p in pts])
+    ref = oracle.conv_points(x, f, b, g, bs, cos, flat)
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        got = y.reshape(B, C_out, Do * Do, 4)[bs, cos, flat]
+        assert_parity(got, ref, what="algo %d" % algo)
