@@ -176,12 +176,67 @@ def cliffconv_cayley_table(k: int, g: Sequence[int]):
 # torch-tensor conveniences (device memory and stream plumbing only).
 # ---------------------------------------------------------------------------
 
-def _check_dev(t, name):
+def _check_dev(t, name, device=None):
+    """t must be a contiguous float32 GPU tensor (on ``device`` if given)."""
     import torch
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise ValueError("%s must be a GPU tensor" % name)
     if t.dtype != torch.float32 or not t.is_contiguous():
         raise ValueError("%s must be contiguous float32" % name)
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, not on %s with the input" % (name, t.device, device))
+
+
+def _check_shape(t, shape, name):
+    """t's full shape must be ``shape`` (checked before any device check, so
+    that a wrong shape is reported as such)."""
+    got = tuple(getattr(t, "shape", ()))
+    if got != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, got, tuple(shape)))
+
+
+def _check_act_arg(act, C: int, nb: int, name: str):
+    """act is None or (mode, blades, weight [C, K] or None, bias [C] or None):
+    blades distinct in [0, N_B); Linear needs both tensors."""
+    if act is None:
+        return
+    mode, blades, aw, ab = act
+    K = len(blades)
+    if not 1 <= K <= nb or len(set(int(b) for b in blades)) != K or \
+            any(not 0 <= int(b) < nb for b in blades):
+        raise ValueError("%s: blades %s must be 1..%d distinct indices in [0, %d)"
+                         % (name, tuple(blades), nb, nb))
+    if mode == AGG_LINEAR:
+        if aw is None or ab is None:
+            raise ValueError("%s: the Linear gate needs a weight and a bias" % name)
+        _check_shape(aw, (C, K), name + " weight")
+        _check_shape(ab, (C,), name + " bias")
+    elif mode not in (AGG_SUM, AGG_MEAN):
+        raise ValueError("%s: unknown aggregation mode %r" % (name, mode))
+
+
+def _check_act_dev(act, device, name):
+    if act is not None and act[0] == AGG_LINEAR:
+        _check_dev(act[2], name + " weight", device)
+        _check_dev(act[3], name + " bias", device)
+
+
+def _conv_dims(x, filters, k: int, name: str = "filters"):
+    """(B, C_in, C_out, d_image, d_filter) of x [B, C_in, d^k, N_B] and
+    filters [C_in, C_out, d_f^k, N_B], with every dimension checked."""
+    nb = 1 << k
+    xs, fs = tuple(getattr(x, "shape", ())), tuple(getattr(filters, "shape", ()))
+    if len(xs) != k + 3 or xs[-1] != nb or len(set(xs[2:-1])) != 1:
+        raise ValueError("x has shape %s, expected [B, C_in] + [d_image] * %d + [%d]"
+                         % (xs, k, nb))
+    B, C_in, d_image = xs[0], xs[1], xs[2]
+    if len(fs) != k + 3 or fs[0] != C_in or fs[-1] != nb or len(set(fs[2:-1])) != 1:
+        raise ValueError("%s has shape %s, expected [%d, C_out] + [d_filter] * %d + [%d]"
+                         % (name, fs, C_in, k, nb))
+    C_out, d_filter = fs[1], fs[2]
+    if d_filter > d_image:
+        raise ValueError("d_filter %d exceeds d_image %d" % (d_filter, d_image))
+    return B, C_in, C_out, d_image, d_filter
 
 
 def _stream_ptr(stream) -> int:
@@ -213,24 +268,29 @@ def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
     [C_in,C_out,d_f^k,N_B] with bias [C_out,N_B] (or None); ``act`` is None or
     (mode, blades, weight [C_out,K] or None, bias [C_out] or None).  Returns
     the output tensor [B,C_out,d_out^k,N_B] (allocated with torch unless
-    ``out`` is given)."""
+    ``out`` is given).  Every tensor's shape, dtype, layout and device is
+    checked before the library is called: the C ABI takes raw pointers and
+    cannot check the buffers behind them."""
     import torch
     k = len(g)
-    _check_dev(x, "x")
-    _check_dev(filters, "filters")
-    if bias is not None:
-        _check_dev(bias, "bias")
-    B, C_in, d_image = x.shape[0], x.shape[1], x.shape[2]
-    C_out, d_filter = filters.shape[1], filters.shape[2]
+    nb = 1 << k
+    B, C_in, C_out, d_image, d_filter = _conv_dims(x, filters, k)
     d_out = d_image - d_filter + 1
-    shape = (B, C_out) + (d_out,) * k + (1 << k,)
+    shape = (B, C_out) + (d_out,) * k + (nb,)
+    if bias is not None:
+        _check_shape(bias, (C_out, nb), "bias")
+    _check_act_arg(act, C_out, nb, "act")
+    if out is not None:
+        _check_shape(out, shape, "out")
+    _check_dev(x, "x")
+    _check_dev(filters, "filters", x.device)
+    if bias is not None:
+        _check_dev(bias, "bias", x.device)
+    _check_act_dev(act, x.device, "act")
     if out is None:
         out = torch.empty(shape, dtype=torch.float32, device=x.device)
-    desc = None
-    if act is not None:
-        mode, blades, aw, ab = act
-        desc = make_act_desc(mode, blades, aw.data_ptr() if aw is not None else 0,
-                             ab.data_ptr() if ab is not None else 0)
+    _check_dev(out, "out", x.device)
+    desc = _act_desc(act)
     st = clifford_conv_nd_algo(k, g, B, C_in, C_out, d_image, d_filter,
                                x.data_ptr(), filters.data_ptr(),
                                bias.data_ptr() if bias is not None else 0,
@@ -243,21 +303,32 @@ def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
 def linear(x, weight, bias, g: Sequence[int], act: Optional[Tuple] = None,
            out=None, stream=None):
     """Clifford linear layer of GPU tensors x [B, C_in, N_B], weight
-    [C_in, C_out, N_B], bias [C_out, N_B] or None; ``act`` as for conv_nd."""
+    [C_in, C_out, N_B], bias [C_out, N_B] or None; ``act`` as for conv_nd.
+    Shapes and devices are checked as in conv_nd."""
     import torch
     k = len(g)
-    _check_dev(x, "x")
-    _check_dev(weight, "weight")
+    nb = 1 << k
+    xs, ws = tuple(getattr(x, "shape", ())), tuple(getattr(weight, "shape", ()))
+    if len(xs) != 3 or xs[-1] != nb:
+        raise ValueError("x has shape %s, expected [B, C_in, %d]" % (xs, nb))
+    B, C_in = xs[0], xs[1]
+    if len(ws) != 3 or ws[0] != C_in or ws[-1] != nb:
+        raise ValueError("weight has shape %s, expected [%d, C_out, %d]" % (ws, C_in, nb))
+    C_out = ws[1]
     if bias is not None:
-        _check_dev(bias, "bias")
-    B, C_in, C_out = x.shape[0], x.shape[1], weight.shape[1]
+        _check_shape(bias, (C_out, nb), "bias")
+    _check_act_arg(act, C_out, nb, "act")
+    if out is not None:
+        _check_shape(out, (B, C_out, nb), "out")
+    _check_dev(x, "x")
+    _check_dev(weight, "weight", x.device)
+    if bias is not None:
+        _check_dev(bias, "bias", x.device)
+    _check_act_dev(act, x.device, "act")
     if out is None:
-        out = torch.empty((B, C_out, 1 << k), dtype=torch.float32, device=x.device)
-    desc = None
-    if act is not None:
-        mode, blades, aw, ab = act
-        desc = make_act_desc(mode, blades, aw.data_ptr() if aw is not None else 0,
-                             ab.data_ptr() if ab is not None else 0)
+        out = torch.empty((B, C_out, nb), dtype=torch.float32, device=x.device)
+    _check_dev(out, "out", x.device)
+    desc = _act_desc(act)
     st = clifford_linear(k, g, B, C_in, C_out, x.data_ptr(), weight.data_ptr(),
                          bias.data_ptr() if bias is not None else 0, out.data_ptr(),
                          desc, _stream_ptr(stream))
@@ -268,17 +339,27 @@ def linear(x, weight, bias, g: Sequence[int], act: Optional[Tuple] = None,
 
 def act_nd(x, mode: int, blades: Sequence[int], weight=None, bias=None,
            out=None, stream=None):
-    """Multivector activation of a GPU tensor [B, C, (positions...), N_B]."""
+    """Multivector activation of a GPU tensor [B, C, (positions...), N_B];
+    weight [C, K] and bias [C] for the Linear gate.  ``out`` may be x (in
+    place).  Shapes and devices are checked before the library is called."""
     import torch
-    _check_dev(x, "x")
-    B, C, nb = x.shape[0], x.shape[1], x.shape[-1]
+    xs = tuple(getattr(x, "shape", ()))
+    if len(xs) < 3 or xs[-1] not in (2, 4, 8):
+        raise ValueError("x has shape %s, expected [B, C, (positions...), N_B] with "
+                         "N_B in (2, 4, 8)" % (xs,))
+    B, C, nb = xs[0], xs[1], xs[-1]
     P = 1
-    for s in x.shape[2:-1]:
+    for s in xs[2:-1]:
         P *= s
+    _check_act_arg((mode, blades, weight, bias), C, nb, "activation")
+    if out is not None:
+        _check_shape(out, xs, "out")
+    _check_dev(x, "x")
+    _check_act_dev((mode, blades, weight, bias), x.device, "activation")
     if out is None:
         out = torch.empty_like(x)
-    desc = make_act_desc(mode, blades, weight.data_ptr() if weight is not None else 0,
-                         bias.data_ptr() if bias is not None else 0)
+    _check_dev(out, "out", x.device)
+    desc = _act_desc((mode, blades, weight, bias))
     st = multivector_act(nb, B, C, P, desc, x.data_ptr(), out.data_ptr(),
                          _stream_ptr(stream))
     if st != CLIFF_OK:
@@ -299,23 +380,50 @@ def block2(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream
     """Two-layer block through clifford_block2_nd: ``layer1``/``layer2`` are
     (filters, bias or None, act or None) as in block_forward.  The workspace
     (B * C_mid * d_mid^k * N_B floats) and the output are allocated with
-    torch unless given."""
+    torch unless given.  Shapes and devices are checked before the library
+    is called."""
     import torch
     k = len(g)
-    (f1, b1, a1), (f2, b2, a2) = layer1, layer2
-    for t, n in ((x, "x"), (f1, "filters1"), (f2, "filters2")):
-        _check_dev(t, n)
-    B, C_in, d_image = x.shape[0], x.shape[1], x.shape[2]
-    C_mid, C_out, d_filter = f1.shape[1], f2.shape[1], f1.shape[2]
-    d_mid = d_image - d_filter + 1
-    d_out = d_mid - d_filter + 1
     nb = 1 << k
+    (f1, b1, a1), (f2, b2, a2) = layer1, layer2
+    B, C_in, C_mid, d_image, d_filter = _conv_dims(x, f1, k, "filters1")
+    d_mid = d_image - d_filter + 1
+    fs2 = tuple(getattr(f2, "shape", ()))
+    if len(fs2) != k + 3 or fs2[0] != C_mid or fs2[2:] != (d_filter,) * k + (nb,):
+        raise ValueError("filters2 has shape %s, expected [%d, C_out] + [%d] * %d + [%d]"
+                         % (fs2, C_mid, d_filter, k, nb))
+    C_out = fs2[1]
+    if d_mid < d_filter:
+        raise ValueError("d_image %d is too small for two layers of d_filter %d"
+                         % (d_image, d_filter))
+    d_out = d_mid - d_filter + 1
+    if b1 is not None:
+        _check_shape(b1, (C_mid, nb), "bias1")
+    if b2 is not None:
+        _check_shape(b2, (C_out, nb), "bias2")
+    _check_act_arg(a1, C_mid, nb, "act1")
+    _check_act_arg(a2, C_out, nb, "act2")
+    ws_shape = (B, C_mid) + (d_mid,) * k + (nb,)
+    out_shape = (B, C_out) + (d_out,) * k + (nb,)
+    if workspace is not None and getattr(workspace, "numel", lambda: -1)() != \
+            B * C_mid * d_mid ** k * nb:
+        raise ValueError("workspace holds %s floats, expected %d (B * C_mid * d_mid^k * N_B)"
+                         % (getattr(workspace, "numel", lambda: None)(),
+                            B * C_mid * d_mid ** k * nb))
+    if out is not None:
+        _check_shape(out, out_shape, "out")
+    _check_dev(x, "x")
+    for t, n in ((f1, "filters1"), (f2, "filters2"), (b1, "bias1"), (b2, "bias2")):
+        if t is not None:
+            _check_dev(t, n, x.device)
+    _check_act_dev(a1, x.device, "act1")
+    _check_act_dev(a2, x.device, "act2")
     if workspace is None:
-        workspace = torch.empty((B, C_mid) + (d_mid,) * k + (nb,), dtype=torch.float32,
-                                device=x.device)
+        workspace = torch.empty(ws_shape, dtype=torch.float32, device=x.device)
     if out is None:
-        out = torch.empty((B, C_out) + (d_out,) * k + (nb,), dtype=torch.float32,
-                          device=x.device)
+        out = torch.empty(out_shape, dtype=torch.float32, device=x.device)
+    _check_dev(workspace, "workspace", x.device)
+    _check_dev(out, "out", x.device)
     st = clifford_block2_nd_path(k, g, B, C_in, C_mid, C_out, d_image, d_filter,
                                  x.data_ptr(), f1.data_ptr(),
                                  b1.data_ptr() if b1 is not None else 0, _act_desc(a1),

@@ -2,21 +2,18 @@
 the launch configuration the benchmark times (clifford_conv_nd, automatic
 kernel choice, activation fused into the convolution for the blocks).
 
-The oracle cannot afford every output at these sizes, so it checks:
-  * the 2D tiny workload and the small block (through the block entry point,
-    fused into one launch) in full;
-  * single convolutions: sampled outputs computed one by one by the oracle
-    (every batch entry, first and last channels, all four/eight borders of the
-    output grid, plus seeded random positions);
-  * blocks (conv -> act -> conv -> act): spatial patches; by translation
-    equivariance (no padding) the block applied to a cropped input equals the
-    same window of the full output, so the oracle runs the whole block, in
-    fp64 end to end, on crops at the corners, edges and interior of every
-    batch entry.
-Gate: normwise relative error <= 1e-4 (see test_parity_gpu).
+Every workload is compared with the fp64 oracle in full except the 3D block
+(8.2 TFLOP, several minutes of oracle time), which is checked on
+  * batch entry 0 in full (the oracle's block on that slice), and
+  * >= 10^5 seeded random (b, c_out, p) outputs across all of B: random
+    (b, p) with every output channel.  The oracle evaluates them as one batch
+    of crops: with no padding the block of the input window that an output
+    reads (d_filter - 1 halo per layer and side) equals that output of the
+    full block (translation equivariance, pinned on the CPU), and batch
+    entries are independent.
+Gate: normwise relative error <= 1e-4; the element-wise relative error over
+|r| >= 1e-3 max|r| is printed beside it (see gpu_util).
 """
-import itertools
-
 import numpy as np
 import pytest
 import torch
@@ -24,7 +21,7 @@ import torch
 import oracle
 import paper_2507_01040_amd as P
 import workloads as W
-from gpu_util import assert_parity, dev
+from gpu_util import assert_parity_report, dev
 
 pytestmark = pytest.mark.gpu
 
@@ -44,25 +41,16 @@ def _gpu_block(w: W.Workload, x, params):
         ts.append((dev(p.filters), dev(p.bias), a))
     y = P.block_forward(xt, ts, w.layers[0].g)
     torch.cuda.synchronize()
-    return y.cpu().numpy()
+    out = y.cpu().numpy()
+    del xt, ts, y
+    torch.cuda.empty_cache()
+    return out
 
 
-def _sample_points(shape: W.ConvShape, n_random: int, seed: int):
-    k, Do = shape.k, shape.d_out
-    pts = []
-    edges = [0, Do - 1]
-    for b in range(shape.B):
-        for co in (0, shape.C_out - 1):
-            for c in itertools.product(edges, repeat=k):
-                pts.append((b, co, c))
-    rng = np.random.default_rng(seed)
-    for _ in range(n_random):
-        pts.append((int(rng.integers(shape.B)), int(rng.integers(shape.C_out)),
-                    tuple(int(v) for v in rng.integers(0, Do, k))))
-    bs = np.array([p[0] for p in pts])
-    cos = np.array([p[1] for p in pts])
-    flat = np.array([int(np.ravel_multi_index(p[2], (Do,) * k)) for p in pts])
-    return bs, cos, flat
+def _oracle_layers(w: W.Workload, params):
+    return [(p.filters, p.bias,
+             None if a is None else (a.mode, a.blades, p.act_weight, p.act_bias))
+            for p, a in zip(params, w.acts)]
 
 
 def test_c1_full():
@@ -70,7 +58,7 @@ def test_c1_full():
     x, ps = W.make_inputs(w)
     y = _gpu_block(w, x, ps)
     ref = oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g)
-    assert_parity(y, ref)
+    assert_parity_report(y, ref, what="conv2d_c4_d16 (full)")
 
 
 def test_small_block_full():
@@ -84,53 +72,64 @@ def test_small_block_full():
                        (act.mode, act.blades, dev(p.act_weight), dev(p.act_bias))))
     y = P.block2(dev(x), layers[0], layers[1], w.layers[0].g)
     torch.cuda.synchronize()
-    ref = oracle.block(x, [(p.filters, p.bias, (a.mode, a.blades, p.act_weight, p.act_bias))
-                           for p, a in zip(ps, w.acts)], w.layers[0].g)
-    assert_parity(y.cpu().numpy(), ref)
+    ref = oracle.block(x, _oracle_layers(w, ps), w.layers[0].g)
+    assert_parity_report(y.cpu().numpy(), ref, what="block2d_c4_d18 (full)")
 
 
+# the fp64 oracle takes up to about a minute on these (all host cores)
+HEAVY = pytest.mark.timeout(600)
+
+
+@HEAVY
 @pytest.mark.parametrize("name", ["conv2d_c64_d128", "conv3d_c32_d32", "conv1d_c64_d60"])
-def test_single_conv_sampled(name):
+def test_single_conv_full(name):
     w = W.WORKLOADS[name]
     x, ps = W.make_inputs(w)
-    shape = w.layers[0]
     y = _gpu_block(w, x, ps)
-    assert np.all(np.isfinite(y))
-    bs, cos, flat = _sample_points(shape, 3000, 5)
-    ref = oracle.conv_points(x, ps[0].filters, ps[0].bias, shape.g, bs, cos, flat)
-    got = y.reshape(shape.B, shape.C_out, -1, shape.nb)[bs, cos, flat]
-    e = assert_parity(got, ref, what=name)
-    print("%s sampled normwise error %.3e over %d outputs" % (name, e, len(bs)))
+    ref = oracle.conv_nd(x, ps[0].filters, ps[0].bias, w.layers[0].g)
+    assert_parity_report(y, ref, what="%s (full)" % name)
 
 
-def _patch_origins(d_final, ps, k, seed):
-    lo, hi = 0, d_final - ps
-    rng = np.random.default_rng(seed)
-    origins = [(lo,) * k, (hi,) * k, tuple([lo] * (k - 1) + [hi]),
-               tuple(int(v) for v in rng.integers(0, hi + 1, k))]
-    return origins
+@HEAVY
+def test_block2d_full():
+    w = W.WORKLOADS["block2d_c64_d130"]
+    x, ps = W.make_inputs(w)
+    y = _gpu_block(w, x, ps)
+    ref = oracle.block(x, _oracle_layers(w, ps), w.layers[0].g)
+    assert_parity_report(y, ref, what="block2d_c64_d130 (full)")
 
 
-@pytest.mark.parametrize("name,ps", [("block2d_c64_d130", 12),
-                                     ("block3d_c64_d36", 4)])
-def test_block_patches(name, ps):
-    w = W.WORKLOADS[name]
-    x, params = W.make_inputs(w)
-    y = _gpu_block(w, x, params)
-    assert np.all(np.isfinite(y))
-    k = w.layers[0].k
+@pytest.fixture(scope="module")
+def block3d():
+    w = W.WORKLOADS["block3d_c64_d36"]
+    x, ps = W.make_inputs(w)
+    y = _gpu_block(w, x, ps)
+    return w, x, ps, y
+
+
+@HEAVY
+def test_block3d_batch0_full(block3d):
+    w, x, ps, y = block3d
+    ref = oracle.block(x[0:1], _oracle_layers(w, ps), w.layers[0].g)
+    assert_parity_report(y[0:1], ref, what="block3d_c64_d36 (batch entry 0 in full)")
+
+
+@HEAVY
+def test_block3d_random_samples(block3d):
+    w, x, ps, y = block3d
+    k, C_out = w.layers[0].k, w.layers[-1].C_out
     halo = sum(l.d_filter - 1 for l in w.layers)
     d_final = w.layers[-1].d_out
-    layers = []
-    for p, a in zip(params, w.acts):
-        layers.append((p.filters, p.bias,
-                       None if a is None else (a.mode, a.blades, p.act_weight, p.act_bias)))
-    worst = 0.0
-    for b in range(w.layers[0].B):
-        for org in _patch_origins(d_final, ps, k, b):
-            crop = (slice(b, b + 1), slice(None)) + tuple(
-                slice(o, o + ps + halo) for o in org)
-            ref = oracle.block(x[crop], layers, w.layers[0].g)
-            win = (slice(b, b + 1), slice(None)) + tuple(slice(o, o + ps) for o in org)
-            worst = max(worst, assert_parity(y[win], ref, what="%s b=%d at %s" % (name, b, org)))
-    print("%s worst patch normwise error %.3e" % (name, worst))
+    n_pos = (100_000 + C_out - 1) // C_out  # (b, p) pairs, every c_out each
+    rng = np.random.default_rng(2024)
+    bs = rng.integers(0, w.layers[0].B, n_pos)
+    org = rng.integers(0, d_final, (n_pos, k))
+    crops = np.stack([x[b][(slice(None),) + tuple(slice(o, o + halo + 1) for o in org[i])]
+                      for i, b in enumerate(bs)])
+    ref = oracle.block(crops, _oracle_layers(w, ps), w.layers[0].g)
+    ref = ref.reshape(n_pos, C_out, -1)
+    got = np.stack([y[b][(slice(None),) + tuple(org[i])] for i, b in enumerate(bs)])
+    assert got.shape == ref.shape
+    assert len(set(bs.tolist())) == w.layers[0].B
+    assert_parity_report(got, ref, what="block3d_c64_d36 (%d random (b, c_out, p) outputs)"
+                         % (n_pos * C_out))
