@@ -288,6 +288,9 @@ cliff_status launch_block_small(const BlockProblem& p, hipStream_t stream)
                 "cliffconv: block_small k=%d bands of %lld slices, %lld workgroups of %d, "
                 "%lld LDS bytes\n",
                 p.k, (long long)R, (long long)n_blk, BS_THREADS, (long long)lds);
+    if (observe_launch(LAUNCH_BLOCK_SMALL, {p.k, p.k == 2 ? 4 : 8, (int)df}, n_blk, BS_THREADS,
+                       lds, &a))
+        return CLIFF_OK;
     auto go = [&](auto kernel) {
         hipLaunchKernelGGL(kernel, dim3((unsigned)n_blk), dim3(BS_THREADS), (size_t)lds, stream,
                            a);

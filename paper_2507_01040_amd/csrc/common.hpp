@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "cliffconv.h"
 
 namespace cliff {
@@ -76,8 +78,56 @@ struct BlockProblem {
 // non-zero value, every launch prints its kernel, grid and tiling to stderr.
 bool debug_enabled();
 
-// Compute units of the current device (cached per device); 0 on error.
+// Compute units of the current device (cached per device); 0 on error.  With
+// a launch observer installed: the observer's count.
 int device_cus();
+
+// Launch observation, for the host-side bounds checker (test
+// infrastructure): a CPU build of the library installs an observer, and every
+// launcher then hands it the launch's plan (kernel, template arguments, grid,
+// workgroup size, LDS bytes, argument block) instead of enqueueing the
+// kernel, and returns CLIFF_OK.  The checker walks the kernel's address
+// arithmetic over every workgroup and lane of the plan.  No observer is ever
+// installed in the library built for the GPU.
+enum LaunchKind {
+    LAUNCH_CONV_MFMA = 1,
+    LAUNCH_CONV1D_MFMA,
+    LAUNCH_CONV_DIRECT,
+    LAUNCH_LINEAR_MFMA,
+    LAUNCH_BLOCK_SMALL,
+    LAUNCH_ACT,
+};
+struct LaunchPlan {
+    int kind;
+    int tpl[12];  // the kernel's template arguments, in declaration order
+    int64_t grid, block, lds_bytes;
+    const void* args;  // the kernel's argument block
+};
+struct LaunchObserver {
+    int cus;  // compute units the dispatch heuristics assume
+    void (*on_launch)(const LaunchPlan& plan, void* ctx);
+    void* ctx;
+};
+extern LaunchObserver* launch_observer;
+
+// Hands the plan to the observer if one is installed (then the caller does
+// not launch).
+inline bool observe_launch(int kind, std::initializer_list<int> tpl, int64_t grid,
+                           int64_t block, int64_t lds_bytes, const void* args)
+{
+    if (!launch_observer) return false;
+    LaunchPlan p;
+    p.kind = kind;
+    int n = 0;
+    for (int v : tpl) p.tpl[n < 12 ? n++ : 11] = v;
+    for (; n < 12; ++n) p.tpl[n] = 0;
+    p.grid = grid;
+    p.block = block;
+    p.lds_bytes = lds_bytes;
+    p.args = args;
+    launch_observer->on_launch(p, launch_observer->ctx);
+    return true;
+}
 
 // host-side launchers (defined in the .hip files)
 cliff_status launch_conv_direct(const ConvProblem& p, hipStream_t stream);

@@ -459,6 +459,9 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
                 "%lld LDS bytes, %d-byte input and %d-byte filter loads\n",
                 (int)df, WCO, WPOS, MW, NW, CO_WG, P, (long long)n_blk, (int)cc,
                 (long long)lds_bytes, 4 * FX, 4 * FW);
+    if (observe_launch(LAUNCH_CONV1D_MFMA, {DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, FX, WK}, n_blk,
+                       NT, lds_bytes, &a))
+        return CLIFF_OK;
     hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, FX, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

@@ -42,6 +42,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "conv_mfma_geom.hpp"
 #include "epilogue.hpp"
 
 #ifndef CLIFF_SGB_IL  // MFMAs between two of the next step's LDS reads; 0: reads clumped
@@ -67,24 +68,6 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-struct MfmaArgs {
-    const float* x;
-    const float* w;
-    const float* bias;
-    float* y;
-    int C_in, C_out, D, Do, df;
-    int M;          // number of output positions B * d_out^k
-    int npos;       // d_out^k
-    int cc;         // input channels per stage
-    int n_stage;    // ceil(C_in / cc) (k = 2) or that times d_filter (k = 3)
-    int n_co_blk, n_blk;
-    int rowblk;     // 2D row-aligned blocks with column-window slabs (wide images)
-    int nseg;       // row-aligned blocks: blocks per output row
-    int sw;         // row-aligned blocks: slab row width in positions
-    int stage_floats;  // LDS floats of one stage buffer
-    SignMasks sign;
-    ActParams act;
-};
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
           int WAVES_PER_SIMD, int WK>
@@ -102,190 +85,59 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 
     extern __shared__ f4 smem4[];
     float* smem = reinterpret_cast<float*>(smem4);
+    constexpr MfmaTile TL{KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK};
 
-    const int df = DF > 0 ? DF : a.df;
-    const int taps2 = df * df;
-    const int taps_full = KD == 2 ? taps2 : taps2 * df;
-    const int D = a.D, Do = a.Do;
-    const int row_floats = D * NB;  // global row stride
-    // Row-aligned blocks (2D images too wide for whole-row slabs): a block is
-    // at most P positions of one output row, and its slab holds only the
-    // d_filter rows x (P + d_filter - 1) columns it reads.
-    const bool rb = KD == 2 && a.rowblk;
-    const int lrow_floats = rb ? a.sw * NB : row_floats;  // LDS slab row
-    const int lrow_f4 = lrow_floats / 4;
+    // Block geometry, staging offsets and fragment offsets: the shared
+    // address arithmetic of conv_mfma_geom.hpp.
+    const MfmaBlock g = mfma_block(TL, a, blockIdx.x);
     const int tid = threadIdx.x;
-
-    // Workgroups are dispatched round-robin over the 8 XCDs; renumber them so
-    // each XCD (own L2) works through a contiguous run of position blocks,
-    // whose input slabs overlap.
-    const int bid = blockIdx.x;
-    const int per = a.n_blk / 8, rem = a.n_blk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    const int tile = xcd < rem ? xcd * (per + 1) + slot
-                               : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int co_blk = tile % a.n_co_blk;
-    const int pos_blk = tile / a.n_co_blk;
-    const int co0 = co_blk * CO_WG;
-    int m0, m_end, x0 = 0;  // x0: first slab column (row-aligned blocks)
-    if (rb) {
-        const int seg = pos_blk % a.nseg, ry = pos_blk / a.nseg;  // output row over (b, y)
-        x0 = seg * P;
-        m0 = ry * Do + x0;
-        m_end = m0 + min(P, Do - x0);
-    } else {
-        m0 = pos_blk * P;
-        m_end = min(m0 + P, a.M);
-    }
-
-    // Slab geometry: output rows r0..r1 (rows of d_out positions), planes
-    // pl0..pl1 (2D: batch entry; 3D: (batch, z)).  Each plane contributes its
-    // output rows plus d_filter - 1 halo rows; full middle planes contribute
-    // all d_image rows.
-    const int r0 = m0 / Do, r1 = (m_end - 1) / Do;
-    const int pl0 = r0 / Do, pl1 = r1 / Do;
-    const int ylo0 = r0 - pl0 * Do;
-    const int len0 = pl0 == pl1 ? (r1 - r0) + df : D - ylo0;
-    const int n_rows = pl0 == pl1 ? len0
-                                  : len0 + (pl1 - pl0 - 1) * D + (r1 - pl1 * Do) + df;
-
-    // Staging.  A stage buffer holds float4 slots in staging order: cc
-    // channel slabs [cc][slab rows] in [0, cc * slab_f4), then cc channels of
-    // filters [cc][co][tap][blade].  Slot t of this lane is buffer float4
-    // f = t * NT + tid, so each wave fills 64 consecutive float4 per slot with
-    // one direct global->LDS load (global_load_lds_dwordx4: lane i lands at
-    // the wave's LDS base + 16 i).  goff >= 0: input float offset from the
-    // stage's slab base; goff < 0: -1 - filter float offset from the stage's
-    // filter base (channels past C_out read the last channel; their results
-    // are never stored).  Slots are channel-major within each section, so a
-    // stage with nv < cc valid channels loads f < nv * slab_f4 (slab) and
-    // f - cc * slab_f4 < nv * wch_f4 (filters).
-    const int cc = CCT > 0 ? CCT : a.cc;  // CCT > 0: channels per stage fixed
-    const int slab_f4 = n_rows * lrow_f4;  // one channel's slab
-    const int wq_f4 = taps2 * NB / 4;
-    const int wch_f4 = CO_WG * wq_f4;     // one channel's filters
-    const int total_f4 = cc * (slab_f4 + wch_f4);
-    const int w_lds = cc * slab_f4 * 4;   // float offset of the filters in a buffer
-    const int b0 = KD == 2 ? pl0 : pl0 / Do;
-    const int z0 = KD == 2 ? 0 : pl0 - b0 * Do;
-    const int plane_floats = D * row_floats;  // one d_image x d_image plane
-    const int x_cstride = plane_floats * (KD == 3 ? D : 1);  // < 2^31 (host check)
-    const int w_cstride = a.C_out * taps_full * NB;
+    const int df = g.df;
+    const int D = g.D;
+    const int cc = g.cc;
+    const int slab_f4 = g.slab_f4;
+    const int wch_f4 = g.wch_f4;
+    const int lrow_floats = g.lrow_floats;
+    const int m0 = g.m0, m_end = g.m_end;
     int goff[SLOTS];
 #pragma unroll
-    for (int t = 0; t < SLOTS; ++t) {
-        const int f = t * NT + tid;
-        goff[t] = 0;
-        if (f < cc * slab_f4) {
-            const int c_l = f / slab_f4;
-            const int fr = f - c_l * slab_f4;
-            const int row = fr / lrow_f4;
-            const int sr = fr - row * lrow_f4;
-            // N_B = 8 rows are stored [half][x][4]: slot sr = half * D + x
-            // holds the global float4 2 x + half of the row; row-aligned
-            // blocks stage columns x0 .. x0 + sw - 1
-            const int col = NB == 8 ? 2 * (sr % D) + sr / D : (rb ? min(x0 + sr, D - 1) : sr);
-            int pl, yin;
-            if (row < len0) {
-                pl = pl0;
-                yin = ylo0 + row;
-            } else {
-                const int s2 = row - len0;
-                pl = pl0 + 1 + s2 / D;
-                yin = s2 - (s2 / D) * D;
-            }
-            int rel;  // planes between pl0's first row and this row's plane
-            if (KD == 2) {
-                rel = (pl - pl0) * a.C_in;
-            } else {
-                const int b = pl / Do, z = pl - (pl / Do) * Do;
-                rel = ((b - b0) * a.C_in * D + (z - z0));
-            }
-            goff[t] = c_l * x_cstride + rel * plane_floats + yin * row_floats + col * 4;
-        } else if (f < total_f4) {
-            const int e = f - cc * slab_f4;
-            const int c_l = e / wch_f4;
-            const int e2 = e - c_l * wch_f4;
-            const int co_l = e2 / wq_f4;
-            const int r4 = e2 - co_l * wq_f4;
-            const int co = min(co0 + co_l, a.C_out - 1);
-            goff[t] = -1 - (c_l * w_cstride + (co - co0) * taps_full * NB + r4 * 4);
-        }
-    }
+    for (int t = 0; t < SLOTS; ++t) goff[t] = mfma_slot_goff(TL, a, g, t * NT + tid);
 
-    const float* xbase = a.x + ((int64_t)b0 * a.C_in * (KD == 3 ? D : 1) + z0) * plane_floats;
-    const float* wbase = a.w + (int64_t)co0 * taps_full * NB;
+    const float* xbase = a.x + mfma_x_base(TL, a, g);
+    const float* wbase = a.w + mfma_w_base(TL, g);
     const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // channels of stage s: [ci0, ci0 + n_valid), filter plane qz
     auto stage_channels = [&](int s, int& ci0, int& qz) {
-        int cg = s;
-        qz = 0;
-        if (KD == 3) {
-            cg = s / df;
-            qz = s - cg * df;
-        }
-        ci0 = cg * cc;
-        return min(cc, a.C_in - ci0);
+        return mfma_stage_channels(TL, a, g, s, ci0, qz);
     };
     auto load_stage = [&](int s, int buf) {
         int ci0, qz;
         const int nv = stage_channels(s, ci0, qz);
-        const float* xs = xbase + (int64_t)ci0 * x_cstride + (int64_t)qz * plane_floats;
-        const float* ws = wbase + (int64_t)ci0 * w_cstride + (int64_t)qz * taps2 * NB;
-        float* lbase = smem + buf * a.stage_floats + wave_u * 256;
+        const float* xs = xbase + mfma_stage_x(g, ci0, qz);
+        const float* ws = wbase + mfma_stage_w(TL, g, ci0, qz);
+        float* lbase = smem + mfma_lds_wave(a, buf, wave_u);
 #pragma unroll
         for (int t = 0; t < SLOTS; ++t) {
-            const int f = t * NT + tid;
-            // with one channel per stage every stage is full
-            const bool load = CCT == 1 ? f < total_f4
-                                       : (goff[t] >= 0 ? f < nv * slab_f4
-                                                       : (f < total_f4 &&
-                                                          f - cc * slab_f4 < nv * wch_f4));
-            if (load) {
+            if (mfma_slot_loads(TL, g, t * NT + tid, goff[t], nv)) {
                 const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
                 __builtin_amdgcn_global_load_lds(
-                    src, (__attribute__((address_space(3))) void*)(lbase + t * NT * 4), 16, 0,
-                    0);
+                    src, (__attribute__((address_space(3))) void*)(lbase + mfma_lds_slot(TL, t)),
+                    16, 0, 0);
             }
         }
     };
 
     // Per-lane constants of the MFMA fragments.
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wk = wave / (WCO * WPOS);     // K slice of this wave
-    const int wrest = wave - wk * (WCO * WPOS);
-    const int wco = wrest % WCO;
-    const int wpos = wrest / WCO;
-    const int mrow = lane & 15;
-    const int kk = lane >> 4;
-
-    // A: row mrow = (output channel co_a, output blade i_a), column kk =
-    // input blade j = 4h + kk.
-    const int co_a = mrow / NB;
-    const int i_a = mrow % NB;
+    const MfmaLane L = mfma_lane(TL, tid);
+    const int lane = L.lane, wk = L.wk, wrest = L.wrest, wco = L.wco, mrow = L.mrow;
     int wofs[NH];
     float sg[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-        const int j = 4 * h + kk;
-        sg[h] = sign_of(a.sign, i_a * NB + j);
-        wofs[h] = w_lds + (wco * MW * CPT + co_a) * taps2 * NB +
-                  src_blade(NB, i_a, j);
+        sg[h] = mfma_a_sign(TL, a, L, h);
+        wofs[h] = mfma_a_ofs(TL, g, L, h);
     }
-    // B: row kk = input blade, column mrow = output position.
     int xoff[NW];
 #pragma unroll
-    for (int nw = 0; nw < NW; ++nw) {
-        int m = m0 + (wpos * NW + nw) * 16 + mrow;
-        m = min(m, m_end - 1);  // tail lanes read a valid position, never stored
-        const int r = m / Do;
-        const int xx = m - r * Do;
-        const int pl = r / Do;
-        const int yy = r - pl * Do;
-        const int srow = pl == pl0 ? yy - ylo0 : len0 + (pl - pl0 - 1) * D + yy;
-        xoff[nw] = srow * lrow_floats + (xx - x0) * 4 + kk;
-    }
+    for (int nw = 0; nw < NW; ++nw) xoff[nw] = mfma_b_ofs(TL, g, L, nw);
 
     f4 acc[MW][NW];
 #pragma unroll
@@ -293,7 +145,6 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #pragma unroll
         for (int nw = 0; nw < NW; ++nw) acc[mw][nw] = f4{0.f, 0.f, 0.f, 0.f};
 
-    const int wtile = CPT * taps2 * NB;  // LDS floats between channel tiles
     auto compute = [&](int buf, int nv) {
       if constexpr (DF > 0) {
         // Software-pipelined over the whole stage: the raw fragments of the
@@ -319,14 +170,13 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         const float* S0 = smem + buf * a.stage_floats;
         float fa[RB][MW], fb[RB][NW];
         auto ld = [&](int c, int u, float(&A)[MW], float(&Bv)[NW]) {
-            const float* S = S0 + c * slab_f4 * 4;
-            const float* Sw = S0 + c * wch_f4 * 4;
+            const float* S = S0 + mfma_b_chan(g, c);
+            const float* Sw = S0 + mfma_a_chan(g, c);
             const int h = u % NH, tap = u / NH, qy = tap / DF, qx = tap % DF;
 #pragma unroll
-            for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[wofs[h] + mw * wtile + tap * NB];
+            for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[mfma_a_tap(TL, g, wofs[h], mw, tap)];
 #pragma unroll
-            for (int nw = 0; nw < NW; ++nw)
-                Bv[nw] = S[xoff[nw] + qy * lrow_floats + h * D * 4 + qx * 4];
+            for (int nw = 0; nw < NW; ++nw) Bv[nw] = S[mfma_b_tap(g, xoff[nw], h, qy, qx)];
         };
         auto chan = [&](int c, auto base_c) {
             constexpr int BASE = decltype(base_c)::value;  // buffer of step 0
@@ -394,10 +244,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         }
       } else {
       for (int c_l = wk; c_l < (CCT > 0 ? CCT : nv); c_l += WK) {
-        // B fragments index S from the channel's slab, A fragments from the
-        // channel's filters (wofs already includes the filter offset)
-        const float* S = smem + buf * a.stage_floats + c_l * slab_f4 * 4;
-        const float* Sw = smem + buf * a.stage_floats + c_l * wch_f4 * 4;
+        const float* S = smem + buf * a.stage_floats + mfma_b_chan(g, c_l);
+        const float* Sw = smem + buf * a.stage_floats + mfma_a_chan(g, c_l);
 #pragma unroll
         for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
             for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
@@ -412,11 +260,10 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
                             float av[MW], bv[NW];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
-                                av[mw] = Sw[wofs[h] + mw * wtile + tap * NB] * sg[h];
+                                av[mw] = Sw[mfma_a_tap(TL, g, wofs[h], mw, tap)] * sg[h];
 #pragma unroll
                             for (int nw = 0; nw < NW; ++nw)
-                                bv[nw] = S[xoff[nw] + qy_ * lrow_floats + h * D * 4 +
-                                           qx_ * 4];
+                                bv[nw] = S[mfma_b_tap(g, xoff[nw], h, qy_, qx_)];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
@@ -449,14 +296,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     if constexpr (WK > 1) {
         // The stage loop ended with a barrier, so LDS is free: K slices
         // 1..WK-1 leave their partial sums there, slice 0 adds them and stores.
-        constexpr int PER = WCO * WPOS * MW * NW;  // f4 per lane per slice
         if (wk > 0) {
 #pragma unroll
             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
                 for (int nw = 0; nw < NW; ++nw)
-                    smem4[((wk - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane] =
-                        acc[mw][nw];
+                    smem4[mfma_red_f4(TL, wk, wrest, mw, nw, lane)] = acc[mw][nw];
         }
         __syncthreads();
         if (wk > 0) return;  // wave-uniform: no barrier follows
@@ -466,14 +311,13 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
                 for (int nw = 0; nw < NW; ++nw)
-                    acc[mw][nw] += smem4[((k - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane];
+                    acc[mw][nw] += smem4[mfma_red_f4(TL, k, wrest, mw, nw, lane)];
     }
 
     // Epilogue: bias, optional multivector activation, 16-byte stores.
-    // D fragment: lane holds rows 4*kk + r of the tile, i.e. output channel
-    // co_o and blades i0..i0+3, for position column mrow.
-    const int co_o = NB == 4 ? kk : (kk >> 1);
-    const int i0 = NB == 4 ? 0 : 4 * (kk & 1);
+    // D fragment: lane holds output channel co and blades i0..i0+3 of one
+    // position.
+    const int i0 = mfma_out_blade0(TL, L);
     const bool has_act = a.act.mode >= 0;
     int gslot[4] = {-1, -1, -1, -1};
     if (has_act) {
@@ -482,7 +326,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     }
 #pragma unroll
     for (int mw = 0; mw < MW; ++mw) {
-        const int co = co0 + (wco * MW + mw) * CPT + co_o;
+        const int co = mfma_out_channel(TL, g, L, mw);
         const bool cvalid = co < a.C_out;
         f4 bb = f4{0.f, 0.f, 0.f, 0.f};
         if (cvalid && a.bias) bb = *reinterpret_cast<const f4*>(a.bias + co * NB + i0);
@@ -493,7 +337,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         }
 #pragma unroll
         for (int nw = 0; nw < NW; ++nw) {
-            const int m = m0 + (wpos * NW + nw) * 16 + mrow;
+            const int m = mfma_out_pos(TL, g, L, nw);
             f4 v = acc[mw][nw] + bb;
             if (has_act) {
                 float part = cf[0] * v[0] + cf[1] * v[1] + cf[2] * v[2] + cf[3] * v[3];
@@ -501,12 +345,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
                 const float gate = cvalid ? gate_sigmoid(a.act, part, co) : 0.f;
                 v *= gate;
             }
-            if (cvalid && m < m_end) {
-                const int b = m / a.npos;
-                const int sp = m - b * a.npos;
-                *reinterpret_cast<f4*>(a.y + (((int64_t)b * a.C_out + co) * a.npos + sp) * NB +
-                                       i0) = v;
-            }
+            if (cvalid && m < m_end)
+                *reinterpret_cast<f4*>(a.y + mfma_out_ofs(TL, a, m, co, i0)) = v;
         }
     }
 }
@@ -618,6 +458,9 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
                 "%d channels/stage, %lld LDS bytes%s\n",
                 KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, WK, (long long)n_blk, (int)cc,
                 (long long)lds_bytes, rowblk ? ", row-aligned blocks" : "");
+    if (observe_launch(LAUNCH_CONV_MFMA, {KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK},
+                       n_blk, NT, lds_bytes, &a))
+        return CLIFF_OK;
     hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

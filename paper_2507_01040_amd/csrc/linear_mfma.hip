@@ -378,6 +378,9 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
                 neg || neg8 ? ", negated weight copy" : "");
     if constexpr (RT == 16 && KQ == 16 && CLIFF_LIN_NEG8) {
         if (neg8 || plain8) {
+            if (observe_launch(LAUNCH_LINEAR_MFMA, {NB, RT, KQ, NWW, PF, WAVES, neg8, 512}, n_wg,
+                               512, lds, &a))
+                return CLIFF_OK;
             if (neg8)
                 hipLaunchKernelGGL((linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, true, 512>),
                                    dim3((unsigned)n_wg), dim3(512), (size_t)lds, stream, a);
@@ -387,6 +390,9 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
             return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
         }
     }
+    if (observe_launch(LAUNCH_LINEAR_MFMA, {NB, RT, KQ, NWW, PF, WAVES, neg, 256}, n_wg, 256, lds,
+                       &a))
+        return CLIFF_OK;
     hipLaunchKernelGGL(neg ? kern_neg : kern, dim3((unsigned)n_wg), dim3(256), (size_t)lds,
                        stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

@@ -1,0 +1,152 @@
+"""Every launch the library would make, checked on the CPU before any GPU
+sees it.
+
+A CPU build of the library (its own host sources, AddressSanitizer and
+UndefinedBehaviorSanitizer on) runs the C ABI entry points with a launch
+observer installed (tests/hostcheck/): argument checks, sign table and kernel
+choice run as on the GPU, and each launch plan goes to a checker that walks
+the kernel's own address arithmetic over every workgroup and lane.  For the
+matrix-core convolution (k = 2, 3) that is every direct global->LDS load in
+bounds, every LDS word a fragment reads written by the stage with the input
+or filter element the product needs, every output stored once in bounds
+(tests/hostcheck/check_conv_mfma.cpp); the other kernels' launch shapes are
+checked for now.
+
+Cases: the GPU parity shapes with every tile shape forced, the benchmark's
+workloads at full size, the random sweeps' draws (convolutions and blocks),
+the block entry point's cases, and wide images.  Each must come back "ok"
+with the status the GPU tests expect (CLIFF_OK, or CLIFF_EUNSUPPORTED for a
+forced tile that refuses a shape).
+"""
+import os
+import sys
+
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+
+import paper_2507_01040_amd as P  # noqa: E402
+import workloads as W  # noqa: E402
+from hostcheck import build as HC  # noqa: E402
+
+ALGOS = [P.ALGO_AUTO, P.ALGO_MFMA, P.ALGO_DIRECT, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM,
+         P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY]
+ALGO_NAMES = dict(zip(ALGOS, ["auto", "mfma", "direct", "wide", "medium", "narrow", "tiny"]))
+
+
+def act_field(act):
+    if act is None:
+        return "-1 0"
+    mode, blades = act[0], act[1]
+    return "%d %d %s" % (mode, len(blades), " ".join(str(b) for b in blades))
+
+
+def conv_line(k, g, B, C_in, C_out, d, df, algo, act=None):
+    return "conv %d %s %d %d %d %d %d %d %s" % (k, " ".join(str(v) for v in g), B, C_in, C_out,
+                                               d, df, algo, act_field(act))
+
+
+def block_line(k, g, B, C_in, C_mid, C_out, d, df, path, act1=None, act2=None):
+    return "block %d %s %d %d %d %d %d %d %d %s %s" % (
+        k, " ".join(str(v) for v in g), B, C_in, C_mid, C_out, d, df, path, act_field(act1),
+        act_field(act2))
+
+
+def _run_cases(cases, allow_unsupported):
+    """cases: (label, line); every result must be ok with CLIFF_OK (or, where
+    allowed, CLIFF_EUNSUPPORTED: a forced tile refusing the shape)."""
+    out = HC.run([line for _, line in cases])
+    assert len(out) == len(cases), out[-5:]
+    bad = []
+    for (label, line), res in zip(cases, out):
+        f = res.split()
+        ok_status = {P.CLIFF_OK} | ({P.CLIFF_EUNSUPPORTED} if allow_unsupported(line) else set())
+        if f[0] != "ok" or int(f[1]) not in ok_status:
+            bad.append("%s: %s" % (label, res[:600]))
+    assert not bad, "\n".join(bad[:20])
+    return out
+
+
+def _is_forced_tile(line):
+    f = line.split()
+    if f[0] != "conv":
+        return False
+    k = int(f[1])
+    algo = int(f[2 + k + 5])
+    return algo >= P.ALGO_MFMA_WIDE
+
+
+def test_parity_shapes_every_tile():
+    import test_parity_gpu as T
+    cases = []
+    for g, shapes in (((1, 1), T.SHAPES2), ((1, 1, 1), T.SHAPES3), ((-1,), T.SHAPES1)):
+        k = len(g)
+        for (B, C_in, C_out, d, df) in shapes:
+            for algo in ALGOS:
+                for act in (None, (P.AGG_LINEAR, tuple(range(1 << k)))):
+                    cases.append(("%s %s %s act=%s" % (g, (B, C_in, C_out, d, df), ALGO_NAMES[algo],
+                                                       act is not None),
+                                  conv_line(k, g, B, C_in, C_out, d, df, algo, act)))
+    _run_cases(cases, _is_forced_tile)
+
+
+def test_benchmark_workloads_full_size():
+    cases = []
+    for name, w in W.WORKLOADS.items():
+        for li, (s, act) in enumerate(zip(w.layers, w.acts)):
+            a = None if act is None else (act.mode, act.blades)
+            for algo in (P.ALGO_AUTO, P.ALGO_MFMA):
+                cases.append(("%s layer %d algo %s" % (name, li, ALGO_NAMES[algo]),
+                              conv_line(s.k, s.g, s.B, s.C_in, s.C_out, s.d_image, s.d_filter,
+                                        algo, a)))
+        if len(w.layers) == 2:
+            s0, s1 = w.layers
+            a0 = None if w.acts[0] is None else (w.acts[0].mode, w.acts[0].blades)
+            a1 = None if w.acts[1] is None else (w.acts[1].mode, w.acts[1].blades)
+            cases.append(("%s block" % name,
+                          block_line(s0.k, s0.g, s0.B, s0.C_in, s0.C_out, s1.C_out, s0.d_image,
+                                     s0.d_filter, P.BLOCK_AUTO, a0, a1)))
+    _run_cases(cases, lambda line: False)
+
+
+def test_random_sweep_draws():
+    import test_random_sweep_gpu as R
+    cases = []
+    for (k, g, B, C_in, C_out, d, df, algo, act, seed) in R.CASES:
+        cases.append((str((k, g, B, C_in, C_out, d, df, algo, act)),
+                      conv_line(k, g, B, C_in, C_out, d, df, algo, act)))
+    _run_cases(cases, _is_forced_tile)
+
+
+def test_block_entry_cases():
+    import test_block_gpu as TB
+    import test_random_block_gpu as RB
+    cases = []
+    for c in TB.CASES:
+        g, B, C_in, C_mid, C_out, d, df, (a1, a2) = c
+        for path in (P.BLOCK_AUTO, P.BLOCK_TWO_LAUNCH, P.BLOCK_FUSED):
+            cases.append((str(c) + " path %d" % path,
+                          block_line(len(g), g, B, C_in, C_mid, C_out, d, df, path, a1, a2)))
+    for c in RB.BLOCKS:
+        g, B, C_in, C_mid, C_out, d, df, (a1, a2) = c[:8]
+        for path in (P.BLOCK_TWO_LAUNCH, P.BLOCK_FUSED):
+            cases.append((str(c) + " path %d" % path,
+                          block_line(len(g), g, B, C_in, C_mid, C_out, d, df, path, a1, a2)))
+    _run_cases(cases, lambda line: int(line.split()[8 + int(line.split()[1])]) == P.BLOCK_FUSED)
+
+
+def test_medium_images_every_tile():
+    # images around the sizes where the wide tiles switch between whole-row
+    # and row-aligned blocks, and the 96-position tile
+    cases = []
+    for d, C, B in ((96, 64, 8), (130, 64, 2), (258, 64, 1), (300, 32, 1), (520, 16, 1),
+                    (1030, 8, 1)):
+        for df in (3, 5):
+            for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_NARROW):
+                cases.append(("2D d %d C %d df %d algo %s" % (d, C, df, ALGO_NAMES[algo]),
+                              conv_line(2, (1, 1), B, C, C, d, df, algo)))
+    for d, C in ((24, 32), (42, 32), (34, 64), (20, 16)):
+        for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM):
+            cases.append(("3D d %d C %d algo %s" % (d, C, ALGO_NAMES[algo]),
+                          conv_line(3, (1, 1, 1), 2, C, C, d, 3, algo)))
+    _run_cases(cases, _is_forced_tile)
