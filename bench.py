@@ -12,7 +12,9 @@ dominant kernel's achieved TFLOP/s (useful FLOPs per launch / its average
 duration from HIP events on the launch stream) against the fp32 matrix-core
 peak.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the
 same workload on this host.  ``workloads`` reports the other workloads the
-same way (3D single conv; 2D/3D blocks with the fused-activation overhead).
+same way (3D single conv; 2D/3D blocks with the fused-activation overhead),
+each with the oracle timed beside it (in full, or the 3D block's first batch
+entry with the whole batch extrapolated).
 """
 from __future__ import annotations
 
@@ -152,14 +154,17 @@ def _device_info(torch):
             "memory_gib": round(pr.total_memory / 2 ** 30, 1)}
 
 
-def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
-    """The fp64 oracle on a bounded sample: the first batch entries of the
-    workload (as many as fit the time budget, at least one)."""
+def cpu_baseline(w: W.Workload, budget_s: float = 12.0, max_entries: int = 0):
+    """The fp64 oracle (all host cores) on the workload's batch entries in
+    order, as many as fit the time budget (None: all of them) or max_entries;
+    at least one.  A sample of fewer than all entries also reports the time
+    of the whole batch extrapolated from it (entries cost the same)."""
     import oracle
     x, params = W.make_inputs(w)
     threads = oracle.default_threads()
+    B = w.layers[0].B
     done_flops, t_total, nb_done = 0, 0.0, 0
-    for b in range(w.layers[0].B):
+    for b in range(B):
         xb = x[b:b + 1]
         t0 = time.perf_counter()
         y = xb
@@ -168,14 +173,27 @@ def cpu_baseline(w: W.Workload, budget_s: float = 12.0):
             if a is not None:
                 y = oracle.act(y, a.mode, a.blades, p.act_weight, p.act_bias)
         t_total += time.perf_counter() - t0
-        done_flops += w.useful_flops // w.layers[0].B
+        done_flops += w.useful_flops // B
         nb_done += 1
-        if t_total >= budget_s:
+        if (budget_s is not None and t_total >= budget_s) or nb_done == max_entries:
             break
-    return {"value": round(done_flops / t_total / 1e9, 3), "unit": "GFLOP/s",
-            "cores": threads, "kind": "oracle",
-            "sample": "%s, batch entries 0..%d of %d (%.2f useful GFLOP), fp64, %.1f s"
-                      % (w.name, nb_done - 1, w.layers[0].B, done_flops / 1e9, t_total)}
+    full = nb_done == B
+    res = {"value": round(done_flops / t_total / 1e9, 3), "unit": "GFLOP/s",
+           "cores": threads, "kind": "oracle",
+           "sample": "%s, %s (%.2f useful GFLOP), fp64, %.1f s"
+                     % (w.name, "whole batch" if full else
+                        "batch entries 0..%d of %d" % (nb_done - 1, B),
+                        done_flops / 1e9, t_total),
+           "seconds": round(t_total, 3)}
+    if not full:
+        res["extrapolated_seconds_whole_batch"] = round(t_total * B / nb_done, 2)
+    return res
+
+
+# The oracle timed beside every workload: in full where it takes well under a
+# minute on the host's cores, else batch entry 0 with the whole batch's time
+# extrapolated (the 3D block: 8.2 TFLOP).
+CPU_BASELINE_PLAN = {"block3d_c64_d36": dict(budget_s=None, max_entries=1)}
 
 
 def _flops(x) -> int:
@@ -443,6 +461,10 @@ def main():
             extra[name] = measure(name, max(3, min(args.steps, 10)), 2,
                                   epilogue_overhead=True)
             torch.cuda.empty_cache()
+        if not args.no_cpu_baseline:
+            for name in extra:
+                extra[name]["cpu_baseline"] = cpu_baseline(
+                    W.WORKLOADS[name], **CPU_BASELINE_PLAN.get(name, dict(budget_s=None)))
         line["workloads"] = extra
         # Clifford linear layers at the paper's C = 32 with GPU-sized batches
         line["clifford_linear"] = [measure_linear(2, 1 << 20, 32), measure_linear(3, 1 << 19, 32),

@@ -28,6 +28,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "conv1d_geom.hpp"
 #include "epilogue.hpp"
 
 #ifndef CLIFF_SGB_IL  // MFMAs between two of the next step's LDS reads; 0: reads clumped
@@ -57,23 +58,6 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-struct C1Args {
-    const float* x;
-    const float* w;
-    const float* bias;
-    float* y;
-    int C_in, C_out, D, Do, df;
-    int M;          // B * d_out flattened output positions
-    int n_co_blk;
-    int n_blk;
-    int cc;         // input channels per stage
-    int ccp;        // channel slots per stage buffer: cc rounded up to even
-    int n_stage;
-    int span2;      // floats per channel window: 2 * (P + rows_max * (d_filter - 1))
-    int stage_floats;
-    SignMasks sign;
-    ActParams act;
-};
 
 template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW, int WAVES, int FW, int FX,
           int WK>
@@ -90,97 +74,35 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
 
     extern __shared__ f4 smem4[];
     float* smem = reinterpret_cast<float*>(smem4);
+    constexpr C1Tile TL{DF, WCO, WPOS, MW, NW, SIN, SW, FW, FX, WK};
 
-    const int df = DF > 0 ? DF : a.df;
-    const int D = a.D, Do = a.Do;
+    // Block geometry, staging and fragment offsets: the shared address
+    // arithmetic of conv1d_geom.hpp.
+    const C1Block g = c1_block(TL, a, blockIdx.x);
+    const int df = g.df;
     const int tid = threadIdx.x;
-
-    // XCD-aware renumbering: consecutive tiles (which share input) go to the
-    // same XCD and its L2.
-    const int bid = blockIdx.x;
-    const int per = a.n_blk / 8, rem = a.n_blk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    const int tile = xcd < rem ? xcd * (per + 1) + slot
-                               : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int co_blk = tile % a.n_co_blk;
-    const int m0 = (tile / a.n_co_blk) * P;
-    const int m_end = min(m0 + P, a.M);
-    const int co0 = co_blk * CO_WG;
-    const int b0 = m0 / Do;
-    // FX = 4 (16-byte input loads, d_image even): the window starts at an
-    // even position, so that every 16-byte piece (two positions) lies inside
-    // one batch entry and is 16-byte aligned in HBM
-    const int x_first = FX == 4 ? (m0 - b0 * Do) & ~1 : m0 - b0 * Do;
-    const int b1 = (m_end - 1) / Do;
-    // window length in positions: (b1 - b0) D + x_last + d_filter - x_first
-    const int span = (b1 - b0) * D + (m_end - 1 - b1 * Do) + df - x_first;
-
-    // Stage buffer (floats): ccp channel windows [ccp][span2], then ccp
-    // channels of filters [ccp][co][tap][2].  Input slot t of this lane covers
-    // window floats FX * (t * NT + tid) onwards (direct loads: lane i lands at
-    // base + 4 FX i): FX = 4 loads two positions at once when d_image is even
-    // (span2 is then a multiple of 4), FX = 1 one float, which needs no
-    // alignment.  Filter slot t covers filter floats FW * (t * NT + tid)
-    // onwards: FW = 4 (16-byte loads) when C_out is even, since then every
-    // channel's chunk of CO_WG x d_filter filters is 16-byte aligned and its
-    // valid part a whole number of 16-byte pieces; FW = 1 otherwise.  The
-    // slots keep 32-bit byte offsets from the stage's uniform base pointers.
+    const int m0 = g.m0, m_end = g.m_end, co0 = g.co0;
     const int span2 = a.span2;
-    const int wch = CO_WG * df * NB;  // floats per channel of filters
-    const int w_lds = a.ccp * span2;
+    const int wch = g.wch;  // floats per channel of filters
+    // 32-bit byte offsets of each slot's source from the stage's bases
     uint32_t xoffb[SIN], woffb[SW];
 #pragma unroll
-    for (int t = 0; t < SIN; ++t) {
-        const int f = (t * NT + tid) * FX;
-        const int c_l = f / span2;
-        const int r = f - c_l * span2;
-        if constexpr (FX == 4) {
-            // an even position; past the window (unused) the last even one,
-            // whose pair is still inside its batch entry (d_image even)
-            const int v = x_first + min(r / NB, (span - 1) & ~1);
-            const int bb = v / D;
-            xoffb[t] = 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB);
-        } else {
-            const int v = x_first + min(r / NB, span - 1);  // past the window: unused
-            const int bb = v / D;
-            xoffb[t] =
-                4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
-        }
-    }
-    // filter floats of a channel chunk that belong to channels < C_out
-    const int wvalid = min(CO_WG, a.C_out - co0) * df * NB;
-    constexpr uint32_t NOLOAD = 0xffffffffu;
+    for (int t = 0; t < SIN; ++t) xoffb[t] = c1_xoffb(TL, a, g, (t * NT + tid) * FX);
 #pragma unroll
-    for (int t = 0; t < SW; ++t) {
-        const int e = (t * NT + tid) * FW;
-        const int c_l = e / wch;
-        const int e2 = e - c_l * wch;
-        if constexpr (FW == 4) {
-            // rows past C_out are not loaded: their stale LDS values only
-            // reach accumulator rows of channels that are never stored
-            woffb[t] = e2 < wvalid ? 4u * (uint32_t)(c_l * a.C_out * df * NB + e2) : NOLOAD;
-        } else {
-            const int co_l = e2 / (df * NB);
-            const int r = e2 - co_l * (df * NB);
-            const int co = min(co0 + co_l, a.C_out - 1);  // past C_out: unused
-            woffb[t] = 4u * (uint32_t)(c_l * a.C_out * df * NB + (co - co0) * df * NB + r);
-        }
-    }
-    const char* xbase = reinterpret_cast<const char*>(a.x + (int64_t)b0 * a.C_in * D * NB);
-    const char* wbase = reinterpret_cast<const char*>(a.w + (int64_t)co0 * df * NB);
+    for (int t = 0; t < SW; ++t) woffb[t] = c1_woffb(TL, a, g, (t * NT + tid) * FW);
+    const char* xbase = reinterpret_cast<const char*>(a.x + c1_x_base(a, g));
+    const char* wbase = reinterpret_cast<const char*>(a.w + c1_w_base(g));
     const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
-    auto stage_channels = [&](int s) { return min(a.cc, a.C_in - s * a.cc); };
+    auto stage_channels = [&](int s) { return c1_stage_channels(a, s); };
     auto load_stage = [&](int s, int buf) {
-        const int ci0 = s * a.cc;
         const int nv = stage_channels(s);
-        const char* xs = xbase + (int64_t)ci0 * D * NB * 4;
-        const char* ws = wbase + (int64_t)ci0 * a.C_out * df * NB * 4;
-        float* lx = smem + buf * a.stage_floats + wave_u * 64 * FX;
-        float* lw = smem + buf * a.stage_floats + w_lds + wave_u * 64 * FW;
+        const char* xs = xbase + c1_stage_x(a, s) * 4;
+        const char* ws = wbase + c1_stage_w(a, g, s) * 4;
 #pragma unroll
         for (int t = 0; t < SIN; ++t) {
-            if ((t * NT + tid) * FX < nv * span2) {
-                auto* dst = (__attribute__((address_space(3))) void*)(lx + t * NT * FX);
+            if (c1_x_loads(a, (t * NT + tid) * FX, nv)) {
+                auto* dst = (__attribute__((address_space(3))) void*)(
+                    smem + c1_lds_x(TL, a, buf, t, wave_u));
                 const float* src = reinterpret_cast<const float*>(xs + xoffb[t]);
                 if constexpr (FX == 4)
                     __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
@@ -190,8 +112,9 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
         }
 #pragma unroll
         for (int t = 0; t < SW; ++t) {
-            if ((t * NT + tid) * FW < nv * wch && (FW == 1 || woffb[t] != NOLOAD)) {
-                auto* dst = (__attribute__((address_space(3))) void*)(lw + t * NT * FW);
+            if (c1_w_loads(TL, g, (t * NT + tid) * FW, woffb[t], nv)) {
+                auto* dst = (__attribute__((address_space(3))) void*)(
+                    smem + c1_lds_w(TL, a, g, buf, t, wave_u));
                 // a float source pointer and literal sizes: with a char
                 // pointer the host pass silently drops the 16-byte form's
                 // kernel stub (undefined symbol at load time)
@@ -204,32 +127,14 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
         }
     };
 
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wk = wave / (WCO * WPOS);  // K slice of this wave
-    const int wrest = wave - wk * (WCO * WPOS);
-    const int wco = wrest % WCO;
-    const int wpos = wrest / WCO;
-    const int mrow = lane & 15;
-    const int kk = lane >> 4;
-    const int c_sub = kk >> 1;  // channel of the pair
-    const int j = kk & 1;       // input blade
-
-    // A: row mrow = (output channel co_a, blade i_a), column (c_sub, j)
-    const int co_a = mrow >> 1;
-    const int i_a = mrow & 1;
-    const float sg = sign_of(a.sign, i_a * NB + j);
-    const int wofs =
-        w_lds + c_sub * wch + (wco * MW * CPT + co_a) * df * NB + src_blade(NB, i_a, j);
-    // B: row (c_sub, j), column mrow = output position
+    const C1Lane L = c1_lane(TL, tid);
+    const int lane = L.lane, wk = L.wk, wrest = L.wrest, wco = L.wco, kk = L.kk;
+    const int c_sub = L.c_sub;
+    const float sg = c1_a_sign(a, L);
+    const int wofs = c1_a_ofs(TL, g, L);
     int xoff[NW];
 #pragma unroll
-    for (int nw = 0; nw < NW; ++nw) {
-        // tail lanes read a valid position; their outputs are not stored
-        const int m = min(m0 + (wpos * NW + nw) * 16 + mrow, m_end - 1);
-        const int bb = m / Do;
-        xoff[nw] = c_sub * span2 + ((bb - b0) * D + (m - bb * Do) - x_first) * NB + j;
-    }
+    for (int nw = 0; nw < NW; ++nw) xoff[nw] = c1_b_ofs(TL, a, g, L, nw);
 
     f4 acc[MW][NW];
 #pragma unroll
@@ -243,12 +148,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     auto pair = [&](const float* S0, int c_l, auto masked) {
         constexpr bool MASKED = decltype(masked)::value;
         const bool on = !MASKED || c_sub == 0;
-        const float* S = S0 + c_l * span2;
-        const float* Sw = S0 + c_l * wch;
+        const float* S = S0 + c1_b_pair(a, c_l);
+        const float* Sw = S0 + c1_a_pair(g, c_l);
         float ar[MW], br[NW];  // raw fragments of the next tap
         auto read = [&](int tap) {
 #pragma unroll
-            for (int mw = 0; mw < MW; ++mw) ar[mw] = Sw[wofs + mw * CPT * df * NB + tap * NB];
+            for (int mw = 0; mw < MW; ++mw) ar[mw] = Sw[c1_a_step(g, wofs, mw, tap)];
 #pragma unroll
             for (int nw = 0; nw < NW; ++nw) br[nw] = S[xoff[nw] + tap * NB];
         };
@@ -323,14 +228,12 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     if constexpr (WK > 1) {
         // The stage loop ended with a barrier, so LDS is free: K slices
         // 1..WK-1 leave their partial sums there, slice 0 adds them and stores.
-        constexpr int PER = WCO * WPOS * MW * NW;  // f4 per lane per slice
         if (wk > 0) {
 #pragma unroll
             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
                 for (int nw = 0; nw < NW; ++nw)
-                    smem4[((wk - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane] =
-                        acc[mw][nw];
+                    smem4[c1_red_f4(TL, wk, wrest, mw, nw, lane)] = acc[mw][nw];
         }
         __syncthreads();
         if (wk > 0) return;  // wave-uniform: no barrier follows
@@ -340,7 +243,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
                 for (int nw = 0; nw < NW; ++nw)
-                    acc[mw][nw] += smem4[((k - 1) * PER + (wrest * MW + mw) * NW + nw) * 64 + lane];
+                    acc[mw][nw] += smem4[c1_red_f4(TL, k, wrest, mw, nw, lane)];
     }
 
     // Epilogue: lane row 4 kk + r is channel 2 kk + r / 2, blade r % 2.
@@ -354,16 +257,15 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     bool mvalid[NW];
 #pragma unroll
     for (int nw = 0; nw < NW; ++nw) {
-        const int m = m0 + (wpos * NW + nw) * 16 + mrow;
+        const int m = c1_out_pos(TL, g, L, nw);
         mvalid[nw] = m < m_end;
-        const int bb = m / Do;
-        ybase[nw] = ((int64_t)bb * a.C_out * Do + (m - bb * Do)) * NB;
+        ybase[nw] = c1_out_base(a, m);
     }
 #pragma unroll
     for (int mw = 0; mw < MW; ++mw) {
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-            const int co = co0 + (wco * MW + mw) * CPT + 2 * kk + half;
+            const int co = c1_out_channel(TL, g, L, mw, half);
             const bool cvalid = co < a.C_out;
             float bias0 = 0.f, bias1 = 0.f, cf0 = 0.f, cf1 = 0.f;
             if (cvalid && a.bias) {
@@ -384,7 +286,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
                     v1 *= g;
                 }
                 if (cvalid && mvalid[nw]) {
-                    float* yp = a.y + ybase[nw] + (int64_t)co * Do * NB;
+                    float* yp = a.y + ybase[nw] + c1_out_chan(a, co);
                     *reinterpret_cast<float2*>(yp) = make_float2(v0, v1);
                 }
             }

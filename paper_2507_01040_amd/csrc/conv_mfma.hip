@@ -63,6 +63,9 @@
 #ifndef CLIFF_SHAPE_MODEL  // quantisation model for the tile choice of large problems
 #define CLIFF_SHAPE_MODEL 1
 #endif
+#ifndef CLIFF_CONV_NEG  // negated filter copy in LDS instead of sign multiplies (wide 3x3(x3) tiles)
+#define CLIFF_CONV_NEG 1
+#endif
 namespace cliff {
 namespace {
 
@@ -70,13 +73,16 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
-          int WAVES_PER_SIMD, int WK>
+          int WAVES_PER_SIMD, int WK, bool NEG>
 __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfma_kernel(
     MfmaArgs a)
 {
     // WK > 1: WK waves share every output tile, each taking every WK-th input
     // channel of a stage; their partial sums meet in LDS before the epilogue
     static_assert(WK == 1 || CCT != 1, "a K split needs several channels per stage");
+    // NEG: negated filter copy in LDS instead of sign multiplies; one channel
+    // per stage, unrolled taps
+    static_assert(!NEG || (CCT == 1 && DF > 0 && WK == 1), "the negated copy needs CCT = 1");
     constexpr int NT = 64 * WCO * WPOS * WK;
     constexpr int CPT = 16 / NB;  // output channels per 16-row tile
     constexpr int CO_WG = WCO * MW * CPT;
@@ -85,7 +91,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 
     extern __shared__ f4 smem4[];
     float* smem = reinterpret_cast<float*>(smem4);
-    constexpr MfmaTile TL{KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK};
+    constexpr MfmaTile TL{KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK, NEG};
+    constexpr int FS = TL.fslots();  // NEG: filter float4 per lane and stage
 
     // Block geometry, staging offsets and fragment offsets: the shared
     // address arithmetic of conv_mfma_geom.hpp.
@@ -125,6 +132,37 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         }
     };
 
+    // NEG: the stage's filters go through registers (global loads issued
+    // with the stage's direct loads, before its predecessor is multiplied),
+    // then to LDS as they are and negated, after the wait that ends the
+    // predecessor (the buffer was last read before the previous barrier).
+    f4 wreg[FS > 0 ? FS : 1];
+    int wsrc[FS > 0 ? FS : 1];
+#pragma unroll
+    for (int u = 0; u < FS; ++u) {
+        const int e = u * NT + tid;
+        wsrc[u] = e < cc * wch_f4 ? mfma_filter_src(TL, a, g, e) : 0;
+    }
+    auto load_filters = [&](int s) {
+        int ci0, qz;
+        stage_channels(s, ci0, qz);
+        const float* ws = wbase + mfma_stage_w(TL, g, ci0, qz);
+#pragma unroll
+        for (int u = 0; u < FS; ++u)
+            if (u * NT + tid < cc * wch_f4) wreg[u] = *reinterpret_cast<const f4*>(ws + wsrc[u]);
+    };
+    auto store_filters = [&](int buf) {
+        float* lw = smem + buf * a.stage_floats;
+#pragma unroll
+        for (int u = 0; u < FS; ++u) {
+            const int e = u * NT + tid;
+            if (e < cc * wch_f4) {
+                *reinterpret_cast<f4*>(lw + mfma_wreg_lds(g, e, 0)) = wreg[u];
+                *reinterpret_cast<f4*>(lw + mfma_wreg_lds(g, e, 1)) = -wreg[u];
+            }
+        }
+    };
+
     // Per-lane constants of the MFMA fragments.
     const MfmaLane L = mfma_lane(TL, tid);
     const int lane = L.lane, wk = L.wk, wrest = L.wrest, wco = L.wco, mrow = L.mrow;
@@ -133,7 +171,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
         sg[h] = mfma_a_sign(TL, a, L, h);
-        wofs[h] = mfma_a_ofs(TL, g, L, h);
+        wofs[h] = mfma_a_ofs(TL, a, g, L, h);
     }
     int xoff[NW];
 #pragma unroll
@@ -169,14 +207,18 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         const int ncl = CCT > 0 ? CCT : nv;
         const float* S0 = smem + buf * a.stage_floats;
         float fa[RB][MW], fb[RB][NW];
+        // (the step offsets take the block's strides as plain values: read
+        // through the block struct inside this lambda, LLVM kept extra
+        // address registers live in the loop, measured 1-3.6 % slower)
         auto ld = [&](int c, int u, float(&A)[MW], float(&Bv)[NW]) {
-            const float* S = S0 + mfma_b_chan(g, c);
-            const float* Sw = S0 + mfma_a_chan(g, c);
+            const float* S = S0 + mfma_b_chan(slab_f4, c);
+            const float* Sw = S0 + mfma_a_chan(wch_f4, c);
             const int h = u % NH, tap = u / NH, qy = tap / DF, qx = tap % DF;
 #pragma unroll
-            for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[mfma_a_tap(TL, g, wofs[h], mw, tap)];
+            for (int mw = 0; mw < MW; ++mw) A[mw] = Sw[mfma_a_tap(TL, DF * DF, wofs[h], mw, tap)];
 #pragma unroll
-            for (int nw = 0; nw < NW; ++nw) Bv[nw] = S[mfma_b_tap(g, xoff[nw], h, qy, qx)];
+            for (int nw = 0; nw < NW; ++nw)
+                Bv[nw] = S[mfma_b_tap(lrow_floats, D, xoff[nw], h, qy, qx)];
         };
         auto chan = [&](int c, auto base_c) {
             constexpr int BASE = decltype(base_c)::value;  // buffer of step 0
@@ -194,7 +236,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #endif
                 float as[MW];
 #pragma unroll
-                for (int mw = 0; mw < MW; ++mw) as[mw] = fa[cur][mw] * sg[u % NH];
+                for (int mw = 0; mw < MW; ++mw) as[mw] = NEG ? fa[cur][mw] : fa[cur][mw] * sg[u % NH];
 #pragma unroll
                 for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
@@ -204,7 +246,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #if CLIFF_SGB_IL
                 // the sign multiplies first, then the next step's LDS reads
                 // spread between this step's MFMAs
-                __builtin_amdgcn_sched_group_barrier(0x002, MW, 0);
+                if (!NEG) __builtin_amdgcn_sched_group_barrier(0x002, MW, 0);
 #pragma unroll
                 for (int r = 0; r < MW + NW; ++r) {
                     __builtin_amdgcn_sched_group_barrier(0x008, CLIFF_SGB_IL, 0);
@@ -244,8 +286,8 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         }
       } else {
       for (int c_l = wk; c_l < (CCT > 0 ? CCT : nv); c_l += WK) {
-        const float* S = smem + buf * a.stage_floats + mfma_b_chan(g, c_l);
-        const float* Sw = smem + buf * a.stage_floats + mfma_a_chan(g, c_l);
+        const float* S = smem + buf * a.stage_floats + mfma_b_chan(slab_f4, c_l);
+        const float* Sw = smem + buf * a.stage_floats + mfma_a_chan(wch_f4, c_l);
 #pragma unroll
         for (int qy = 0; qy < (DF > 0 ? DF : 1); ++qy) {
             for (int qyr = 0; qyr < (DF > 0 ? 1 : df); ++qyr) {
@@ -260,10 +302,10 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
                             float av[MW], bv[NW];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
-                                av[mw] = Sw[mfma_a_tap(TL, g, wofs[h], mw, tap)] * sg[h];
+                                av[mw] = Sw[mfma_a_tap(TL, df * df, wofs[h], mw, tap)] * sg[h];
 #pragma unroll
                             for (int nw = 0; nw < NW; ++nw)
-                                bv[nw] = S[mfma_b_tap(g, xoff[nw], h, qy_, qx_)];
+                                bv[nw] = S[mfma_b_tap(lrow_floats, D, xoff[nw], h, qy_, qx_)];
 #pragma unroll
                             for (int mw = 0; mw < MW; ++mw)
 #pragma unroll
@@ -282,14 +324,21 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     // Main loop: one barrier per stage; the next stage's global loads are in
     // flight while the current one is multiplied.
     load_stage(0, 0);
+    if constexpr (NEG) load_filters(0);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if constexpr (NEG) store_filters(0);
     __syncthreads();
     for (int s = 0; s < a.n_stage; ++s) {
         // buffer (s+1)&1 was last read in iteration s-1, before the barrier
-        if (s + 1 < a.n_stage) load_stage(s + 1, (s + 1) & 1);
+        if (s + 1 < a.n_stage) {
+            load_stage(s + 1, (s + 1) & 1);
+            if constexpr (NEG) load_filters(s + 1);
+        }
         int ci0, qz;
         compute(s & 1, stage_channels(s, ci0, qz));
         __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if constexpr (NEG)
+            if (s + 1 < a.n_stage) store_filters((s + 1) & 1);
         __syncthreads();
     }
 
@@ -356,7 +405,7 @@ struct TileCfg {
 };
 
 template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, int SLOTS,
-          int WAVES, int WK, int LDSKB>
+          int WAVES, int WK, int LDSKB, bool NEG>
 cliff_status run(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int NT = 64 * WCO * WPOS * WK;
@@ -369,27 +418,32 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     const int64_t M = p.B * npos;
     int64_t n_pos_blk = (M + P - 1) / P;
     const int64_t n_co_blk = (p.C_out + CO_WG - 1) / CO_WG;
-    if (M >= (1ll << 31) || D * D * NB >= (1 << 24)) return CLIFF_EUNSUPPORTED;
+    // 32-bit position indices; one d_image^2 plane of floats in 32 bits
+    if (M >= (1ll << 31) || D * D * NB >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
     // Upper bound of the slab rows of any block.
     const int64_t total_rows = M / Do;
     const int64_t R = std::min<int64_t>((P - 1) / Do + 2, total_rows);
     const int64_t planes = std::min<int64_t>(R, (R - 1) / Do + 2);
     const int64_t rows_max = R + planes * (df - 1);
-    int64_t ch_floats = rows_max * D * NB + CO_WG * df * df * NB;  // per channel
+    // per channel: LDS floats (slab, filters, NEG: negated filters) and the
+    // floats staged by direct loads (NEG: the slab only)
+    const int64_t wch = CO_WG * df * df * NB;
+    int64_t ch_floats = rows_max * D * NB + (NEG ? 2 : 1) * wch;
+    int64_t ch_dma = rows_max * D * NB + (NEG ? 0 : wch);
     // Channels per stage: enough MFMAs per wave between barriers, within the
     // LDS budget (two buffers) and the staging slots.
     constexpr int64_t LDS_BUDGET = LDSKB * 1024;
     constexpr int64_t MFMA_PER_STAGE = 512;
     const int64_t mfma_per_ch = df * df * (NB / 4) * MW * NW;
-    auto channels = [&](int64_t chf) {
+    auto channels = [&](int64_t chf, int64_t chd) {
         int64_t c = std::min<int64_t>(p.C_in, (MFMA_PER_STAGE + mfma_per_ch - 1) / mfma_per_ch);
         c = std::min<int64_t>(c, LDS_BUDGET / (2 * chf * 4));
-        c = std::min<int64_t>(c, (int64_t)SLOTS * NT / (chf / 4));
+        c = std::min<int64_t>(c, (int64_t)SLOTS * NT / (chd / 4));
         if (CCT > 0) c = c >= CCT ? CCT : 0;
         if (WK > 1 && c > WK) c -= c % WK;  // equal channel shares for the K slices
         return c;
     };
-    int64_t cc = channels(ch_floats);
+    int64_t cc = channels(ch_floats, ch_dma);
     // Row-aligned blocks with column-window slabs (d_filter rows of
     // min(P, d_out) + d_filter - 1 positions): for 2D images whose whole-row
     // slabs do not fit, and on the wide tiles wherever a row's blocks leave
@@ -403,17 +457,20 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     if (KD == 2 && (CLIFF_ROWBLK == 2 || (p.rowblk == 2 && snug) ||
                     (cc < 1 && CLIFF_ROWBLK == 1 && p.rowblk == 1))) {
         sw = std::min<int64_t>(P, Do) + df - 1;
-        const int64_t chf = df * sw * NB + CO_WG * df * df * NB;
-        const int64_t c = channels(chf);
+        const int64_t chf = df * sw * NB + (NEG ? 2 : 1) * wch;
+        const int64_t chd = df * sw * NB + (NEG ? 0 : wch);
+        const int64_t c = channels(chf, chd);
         if (c >= 1) {
             ch_floats = chf;
+            ch_dma = chd;
             cc = c;
             nseg = (Do + P - 1) / P;
             n_pos_blk = p.B * Do * nseg;
             rowblk = 1;
         }
     }
-    if (cc < 1) return CLIFF_EUNSUPPORTED;
+    if (cc < 1 || (NEG && cc != 1)) return CLIFF_EUNSUPPORTED;
+    (void)ch_dma;
     const int64_t n_blk = n_pos_blk * n_co_blk;
     if (n_blk >= (1ll << 31)) return CLIFF_EUNSUPPORTED;
     const int64_t stage_floats = cc * ch_floats;
@@ -424,7 +481,12 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     // staging offsets are 32-bit, relative to the block's first plane
     int64_t img = NB;
     for (int t = 0; t < KD; ++t) img *= D;
-    if ((cc + (planes + 2) * p.C_in) * img >= (1ll << 31) ||
+    // flattened blocks: planes of several batch entries, offsets relative to
+    // the first (and images below 2^24 floats per plane); row-aligned
+    // blocks: rows of one plane, cc channels from the block's first
+    if ((!rowblk && (D * D * NB >= (1 << 24) ||
+                     (cc + (planes + 2) * p.C_in) * img >= (1ll << 31))) ||
+        (rowblk && (cc + 1) * img >= (1ll << 31)) ||
         cc * p.C_out * df * df * (KD == 3 ? df : 1) * NB >= (1ll << 31))
         return CLIFF_EUNSUPPORTED;
 
@@ -455,13 +517,15 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
         fprintf(stderr,
                 "cliffconv: conv_mfma k=%d d_filter=%d tile %dx%d waves of %dx%d MFMA tiles "
                 "(%d channels x %d positions), K split over %d waves, %lld workgroups, "
-                "%d channels/stage, %lld LDS bytes%s\n",
+                "%d channels/stage, %lld LDS bytes%s%s\n",
                 KD, (int)df, WCO, WPOS, MW, NW, CO_WG, P, WK, (long long)n_blk, (int)cc,
-                (long long)lds_bytes, rowblk ? ", row-aligned blocks" : "");
-    if (observe_launch(LAUNCH_CONV_MFMA, {KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK},
-                       n_blk, NT, lds_bytes, &a))
+                (long long)lds_bytes, rowblk ? ", row-aligned blocks" : "",
+                NEG ? ", negated filter copy" : "");
+    if (observe_launch(LAUNCH_CONV_MFMA,
+                       {KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, NEG}, n_blk, NT,
+                       lds_bytes, &a))
         return CLIFF_OK;
-    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK>),
+    hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, NEG>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
 }
@@ -522,7 +586,13 @@ template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, in
 cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream,
                            Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB>)
 {
-    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB>(p, stream);
+    // one channel per stage and no zero sign in the table: the negated filter
+    // copy replaces the sign multiplies
+    if constexpr (CCT == 1 && DF > 0 && WK == 1 && CLIFF_CONV_NEG)
+        if (p.sign.zero == 0)
+            return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB, true>(p,
+                                                                                         stream);
+    return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB, false>(p, stream);
 }
 
 template <int KD, int NB, int DF, class Wide, class... WideAlt>

@@ -34,14 +34,22 @@ struct MfmaArgs {
 // The compile-time shape of one kernel instantiation, as plain ints: KD
 // spatial dimensions, NB blades, DF filter size (0: run time), CCT channels
 // per stage (0: run time), WCO x WPOS waves of MW x NW MFMA tiles (16 x 16),
-// SLOTS staging slots per lane, the K loop split over WK waves.
+// SLOTS staging slots per lane, the K loop split over WK waves.  NEG: the
+// filters are staged through registers, as they are and negated (two LDS
+// copies), and each A lane reads the copy of its table sign instead of
+// multiplying by it (one channel per stage, no zero sign).
 struct MfmaTile {
-    int KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK;
+    int KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK, NEG;
     __host__ __device__ constexpr int nt() const { return 64 * WCO * WPOS * WK; }
     __host__ __device__ constexpr int cpt() const { return 16 / NB; }  // channels per tile
     __host__ __device__ constexpr int co_wg() const { return WCO * MW * (16 / NB); }
     __host__ __device__ constexpr int pos() const { return WPOS * NW * 16; }
     __host__ __device__ constexpr int nh() const { return NB / 4; }  // 4-blade groups
+    // NEG: float4 of filters per lane and stage (filter registers)
+    __host__ __device__ constexpr int fslots() const
+    {
+        return NEG ? (co_wg() * DF * DF * NB / 4 + nt() - 1) / nt() : 0;
+    }
 };
 
 // Geometry of one workgroup's block: P consecutive flattened output positions
@@ -54,7 +62,7 @@ struct MfmaBlock {
     int b0, z0;                   // batch entry (and, for k = 3, plane) of the first row
     int df, taps2, taps_full, D, Do;
     int row_floats, lrow_floats;  // global and LDS row strides
-    int cc, slab_f4, wq_f4, wch_f4, total_f4, w_lds;
+    int cc, slab_f4, wq_f4, wch_f4, total_f4, w_lds, w_neg;
     int plane_floats, x_cstride, w_cstride;
     bool rb;
 };
@@ -108,8 +116,10 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     g.slab_f4 = g.n_rows * (g.lrow_floats / 4);  // one channel's slab
     g.wq_f4 = g.taps2 * NB / 4;
     g.wch_f4 = T.co_wg() * g.wq_f4;              // one channel's filters
-    g.total_f4 = g.cc * (g.slab_f4 + g.wch_f4);
+    // float4 staged by direct loads (NEG: the slabs only)
+    g.total_f4 = g.cc * (g.slab_f4 + (T.NEG ? 0 : g.wch_f4));
     g.w_lds = g.cc * g.slab_f4 * 4;              // float offset of the filters in a buffer
+    g.w_neg = g.w_lds + g.cc * g.wch_f4 * 4;     // NEG: of their negated copy
     g.b0 = T.KD == 2 ? g.pl0 : g.pl0 / Do;
     g.z0 = T.KD == 2 ? 0 : g.pl0 - g.b0 * Do;
     g.plane_floats = D * g.row_floats;           // one d_image x d_image plane
@@ -118,9 +128,32 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     return g;
 }
 
+// Float offset, from the stage's filter base, of float4 e of the stage's
+// filters [cc][co][tap][blade] in LDS order (channels past C_out read the
+// last channel; their results are never stored).
+__host__ __device__ inline int mfma_filter_src(const MfmaTile& T, const MfmaArgs& a,
+                                               const MfmaBlock& g, int e)
+{
+    const int c_l = e / g.wch_f4;
+    const int e2 = e - c_l * g.wch_f4;
+    const int co_l = e2 / g.wq_f4;
+    const int r4 = e2 - co_l * g.wq_f4;
+    const int co = g.co0 + co_l < a.C_out - 1 ? g.co0 + co_l : a.C_out - 1;
+    return c_l * g.w_cstride + (co - g.co0) * g.taps_full * T.NB + r4 * 4;
+}
+
+// NEG: filter register slot u of lane tid holds float4 e = u * NT + tid of
+// the stage's filters (when e < cc * wch_f4); it is written to LDS at
+// mfma_wreg_lds(g, e, 0) as it is and at mfma_wreg_lds(g, e, 1) negated.
+__host__ __device__ inline int mfma_wreg_lds(const MfmaBlock& g, int e, int neg)
+{
+    return (neg ? g.w_neg : g.w_lds) + 4 * e;
+}
+
 // Staging.  A stage buffer holds float4 slots in staging order: cc channel
 // slabs [cc][slab rows] in [0, cc * slab_f4), then cc channels of filters
-// [cc][co][tap][blade].  Float4 f = t * NT + tid of the buffer is slot t of
+// [cc][co][tap][blade] (NEG: then their negated copy; the filters do not go
+// through the direct-load slots but through registers, mfma_wreg_*).  Float4 f = t * NT + tid of the buffer is slot t of
 // lane tid.  Returns its source offset: >= 0, the input float offset from the
 // stage's slab base; < 0, -1 - the filter float offset from the stage's filter
 // base (channels past C_out read the last channel; their results are never
@@ -157,15 +190,7 @@ __host__ __device__ inline int mfma_slot_goff(const MfmaTile& T, const MfmaArgs&
         }
         return c_l * g.x_cstride + rel * g.plane_floats + yin * g.row_floats + col * 4;
     }
-    if (f < g.total_f4) {
-        const int e = f - g.cc * g.slab_f4;
-        const int c_l = e / g.wch_f4;
-        const int e2 = e - c_l * g.wch_f4;
-        const int co_l = e2 / g.wq_f4;
-        const int r4 = e2 - co_l * g.wq_f4;
-        const int co = g.co0 + co_l < a.C_out - 1 ? g.co0 + co_l : a.C_out - 1;
-        return -1 - (c_l * g.w_cstride + (co - g.co0) * g.taps_full * NB + r4 * 4);
-    }
+    if (f < g.total_f4) return -1 - mfma_filter_src(T, a, g, f - g.cc * g.slab_f4);
     return 0;
 }
 
@@ -250,12 +275,13 @@ __host__ __device__ inline MfmaLane mfma_lane(const MfmaTile& T, int tid)
 }
 
 // A fragment: buffer float offset of the lane's raw filter blade for blade
-// group h, before the per-step part (mfma_a_step).
-__host__ __device__ inline int mfma_a_ofs(const MfmaTile& T, const MfmaBlock& g,
-                                          const MfmaLane& l, int h)
+// group h (NEG: in the copy of the lane's sign), before the per-step part.
+__host__ __device__ inline int mfma_a_ofs(const MfmaTile& T, const MfmaArgs& a,
+                                          const MfmaBlock& g, const MfmaLane& l, int h)
 {
     const int co_a = l.mrow / T.NB, i_a = l.mrow % T.NB;
-    return g.w_lds + (l.wco * T.MW * T.cpt() + co_a) * g.taps2 * T.NB +
+    const bool neg = T.NEG && sign_of(a.sign, i_a * T.NB + 4 * h + l.kk) < 0.0f;
+    return (neg ? g.w_neg : g.w_lds) + (l.wco * T.MW * T.cpt() + co_a) * g.taps2 * T.NB +
            src_blade(T.NB, i_a, 4 * h + l.kk);
 }
 __host__ __device__ inline float mfma_a_sign(const MfmaTile& T, const MfmaArgs& a,
@@ -264,18 +290,17 @@ __host__ __device__ inline float mfma_a_sign(const MfmaTile& T, const MfmaArgs& 
     const int i_a = l.mrow % T.NB;
     return sign_of(a.sign, i_a * T.NB + 4 * h + l.kk);
 }
-// per step: channel c of the stage (its filters start mfma_a_chan floats
-// into the buffer), then channel tile mw and filter tap (2D index) around the
-// lane's offset
-__host__ __device__ inline int mfma_a_chan(const MfmaBlock& g, int c) { return c * g.wch_f4 * 4; }
-__host__ __device__ inline int mfma_a_tap(const MfmaTile& T, const MfmaBlock& g, int wofs, int mw,
-                                          int tap)
+// per step: channel c of the stage (its filters start mfma_a_chan(wch_f4, c)
+// floats into the buffer), then channel tile mw and filter tap (2D index) around the
+// lane's offset (wtaps: taps per filter plane, d_filter^2)
+__host__ __device__ inline int mfma_a_chan(int wch_f4, int c) { return c * wch_f4 * 4; }
+__host__ __device__ inline int mfma_a_tap(const MfmaTile& T, int wtaps, int wofs, int mw, int tap)
 {
-    return wofs + mw * (T.cpt() * g.taps2 * T.NB) + tap * T.NB;
+    return wofs + mw * (T.cpt() * wtaps * T.NB) + tap * T.NB;
 }
 
 // B fragment: buffer float offset of the lane's input blade kk at output
-// position column nw, before the per-step part (mfma_b_step).  Tail lanes
+// position column nw, before the per-step part (mfma_b_chan, mfma_b_tap).  Tail lanes
 // read a valid position; their outputs are never stored.
 __host__ __device__ inline int mfma_b_ofs(const MfmaTile& T, const MfmaBlock& g,
                                           const MfmaLane& l, int nw)
@@ -290,13 +315,13 @@ __host__ __device__ inline int mfma_b_ofs(const MfmaTile& T, const MfmaBlock& g,
     const int srow = pl == g.pl0 ? yy - g.ylo0 : g.len0 + (pl - g.pl0 - 1) * D + yy;
     return srow * g.lrow_floats + (xx - g.x0) * 4 + l.kk;
 }
-// per step: channel c (its slab starts mfma_b_chan floats into the buffer),
+// per step: channel c (its slab starts mfma_b_chan(slab_f4, c) floats in),
 // then filter row qy and column qx of the tap and blade group h around the
-// lane's offset
-__host__ __device__ inline int mfma_b_chan(const MfmaBlock& g, int c) { return c * g.slab_f4 * 4; }
-__host__ __device__ inline int mfma_b_tap(const MfmaBlock& g, int xoff, int h, int qy, int qx)
+// lane's offset (lrow_floats, D: the block's LDS row stride and d_image)
+__host__ __device__ inline int mfma_b_chan(int slab_f4, int c) { return c * slab_f4 * 4; }
+__host__ __device__ inline int mfma_b_tap(int lrow_floats, int D, int xoff, int h, int qy, int qx)
 {
-    return xoff + qy * g.lrow_floats + h * g.D * 4 + qx * 4;
+    return xoff + qy * lrow_floats + h * D * 4 + qx * 4;
 }
 
 // K split: float4 index in LDS where K slice wk >= 1 leaves tile (mw, nw) of

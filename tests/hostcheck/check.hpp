@@ -27,7 +27,9 @@ struct Case {
     std::vector<Buffer> buffers;
     Dims dims;
     int launches = 0;
-    int64_t workgroups = 0;  // workgroups whose accesses were walked
+    int64_t workgroups = 0;  // workgroups whose LDS image was simulated
+    bool grid_sampled = false;  // a grid too large to walk every workgroup
+    std::string kinds;          // LaunchKind of each launch, comma-separated
     int errors = 0;
     std::string first_error;
 };
@@ -38,6 +40,7 @@ void fail(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 const Buffer* find_buffer(const void* p);
 
 void check_conv_mfma(const cliff::LaunchPlan& p);
+void check_conv1d(const cliff::LaunchPlan& p);
 void check_generic(const cliff::LaunchPlan& p);
 
 }  // namespace hostcheck

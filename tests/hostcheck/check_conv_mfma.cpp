@@ -107,6 +107,39 @@ bool stage_loads(const Ctx& C, const MfmaBlock& g, int s, const std::vector<int>
                 }
             }
         }
+    // NEG: the filters through registers, written as they are and negated
+    for (int u = 0; u < T.fslots(); ++u)
+        for (int tid = 0; tid < NT; ++tid) {
+            const int e = u * NT + tid;
+            if (e >= g.cc * g.wch_f4) continue;
+            const int64_t src = ws + mfma_filter_src(T, a, g, e);
+            if (src < 0 || src + 4 > C.n_w || (src & 3)) {
+                fail("block %d stage %d filter register %d lane %d: load at float %lld of %lld",
+                     bid, s, u, tid, (long long)src, (long long)C.n_w);
+                ok = false;
+                continue;
+            }
+            for (int neg = 0; neg < 2; ++neg) {
+                const int64_t dst = mfma_wreg_lds(g, e, neg);
+                if (dst < 0 || dst + 4 > a.stage_floats ||
+                    ((int64_t)buf * a.stage_floats + dst + 4) * 4 > C.lds_bytes) {
+                    fail("block %d stage %d filter register %d lane %d: LDS write at %lld",
+                         bid, s, u, tid, (long long)dst);
+                    ok = false;
+                    continue;
+                }
+                if (!lds_src) continue;
+                for (int q = 0; q < 4; ++q) {
+                    int64_t& slot = (*lds_src)[dst + q];
+                    if (slot != -1) {
+                        fail("block %d stage %d: LDS float %lld written twice", bid, s,
+                             (long long)(dst + q));
+                        ok = false;
+                    }
+                    slot = ((int64_t)(neg ? 3 : 2) << 60) | (src + q);
+                }
+            }
+        }
     return ok;
 }
 
@@ -154,8 +187,9 @@ void stage_fragments(const Ctx& C, const MfmaBlock& g, int s, const std::vector<
                     const int j = 4 * h + L.kk;
                     // A fragments
                     for (int mw = 0; mw < T.MW; ++mw) {
-                        const int64_t ofs = mfma_a_chan(g, c) +
-                                            mfma_a_tap(T, g, mfma_a_ofs(T, g, L, h), mw, tap);
+                        const int64_t ofs =
+                            mfma_a_chan(g.wch_f4, c) +
+                            mfma_a_tap(T, g.taps2, mfma_a_ofs(T, a, g, L, h), mw, tap);
                         int co = g.co0 + (L.wco * T.MW + mw) * T.cpt() + co_a;
                         if (co >= C.C_out) co = (int)C.C_out - 1;
                         int q[3];
@@ -167,8 +201,10 @@ void stage_fragments(const Ctx& C, const MfmaBlock& g, int s, const std::vector<
                             q[1] = qy;
                             q[2] = qx;
                         }
+                        // kind 3: the negated copy, read by lanes of sign -1 (NEG)
+                        const int64_t kind = T.NEG && mfma_a_sign(T, a, L, h) < 0.f ? 3 : 2;
                         const int64_t want =
-                            ((int64_t)2 << 60) | w_index(C, ci0 + c, co, q, src_blade(NB, i_a, j));
+                            (kind << 60) | w_index(C, ci0 + c, co, q, src_blade(NB, i_a, j));
                         const int64_t got =
                             ofs >= 0 && ofs < (int64_t)lds_src.size() ? lds_src[ofs] : -2;
                         if (got != want) bad("A tile", tid, c, tap, h, mw, ofs, got, want);
@@ -176,7 +212,8 @@ void stage_fragments(const Ctx& C, const MfmaBlock& g, int s, const std::vector<
                     // B fragments
                     for (int nw = 0; nw < T.NW; ++nw) {
                         const int64_t ofs =
-                            mfma_b_chan(g, c) + mfma_b_tap(g, mfma_b_ofs(T, g, L, nw), h, qy, qx);
+                            mfma_b_chan(g.slab_f4, c) +
+                            mfma_b_tap(g.lrow_floats, g.D, mfma_b_ofs(T, g, L, nw), h, qy, qx);
                         int64_t m = g.m0 + (L.wpos * T.NW + nw) * 16 + L.mrow;
                         m = std::min<int64_t>(m, g.m_end - 1);
                         const int64_t b = m / C.npos;
@@ -205,8 +242,8 @@ void stage_fragments(const Ctx& C, const MfmaBlock& g, int s, const std::vector<
 void check_conv_mfma(const LaunchPlan& p)
 {
     Ctx C;
-    C.T = MfmaTile{p.tpl[0], p.tpl[1], p.tpl[2], p.tpl[3], p.tpl[4],
-                   p.tpl[5], p.tpl[6], p.tpl[7], p.tpl[8], p.tpl[10]};
+    C.T = MfmaTile{p.tpl[0], p.tpl[1], p.tpl[2], p.tpl[3], p.tpl[4], p.tpl[5],
+                   p.tpl[6], p.tpl[7], p.tpl[8], p.tpl[10], p.tpl[11]};
     const MfmaTile& T = C.T;
     const MfmaArgs& a = *static_cast<const MfmaArgs*>(p.args);
     C.a = &a;
@@ -259,16 +296,23 @@ void check_conv_mfma(const LaunchPlan& p)
     const int64_t stride = std::max<int64_t>(1, (p.grid * per_block * 2) / budget);
 
     std::vector<uint8_t> written((size_t)(C.n_y / 4), 0);
+    current->grid_sampled |= (p.grid >> 15) > 1;
     std::vector<int> goff((size_t)T.SLOTS * NT);
     std::vector<int64_t> lds_src;
+    // grids of more than 2^15 workgroups: every (grid / 2^15)-th one, the
+    // first and the last 64 (and no output coverage count)
+    const int64_t wstride = std::max<int64_t>(1, p.grid >> 15);
     for (int bid = 0; bid < p.grid; ++bid) {
+        if (wstride > 1 && bid % wstride && bid >= 64 && bid < p.grid - 64) continue;
         const MfmaBlock g = mfma_block(T, a, bid);
         if (g.m0 < 0 || g.m_end > a.M || g.m0 >= g.m_end || g.co0 < 0 || g.co0 >= a.C_out) {
             fail("block %d covers positions [%d, %d) of %d, channels from %d", bid, g.m0, g.m_end,
                  a.M, g.co0);
             continue;
         }
-        if ((int64_t)g.total_f4 * 4 > a.stage_floats || (int64_t)T.SLOTS * NT < g.total_f4)
+        if ((int64_t)g.total_f4 * 4 > a.stage_floats || (int64_t)T.SLOTS * NT < g.total_f4 ||
+            (T.NEG && (g.cc != 1 || (int64_t)T.fslots() * NT < g.wch_f4 ||
+                       g.w_neg + g.cc * g.wch_f4 * 4 > a.stage_floats)))
             fail("block %d stages %d float4 in %d slots of a %d-float buffer", bid, g.total_f4,
                  T.SLOTS * NT, a.stage_floats);
         for (int t = 0; t < T.SLOTS; ++t)
@@ -337,7 +381,7 @@ void check_conv_mfma(const LaunchPlan& p)
         }
         if (current->errors >= 8) return;
     }
-    for (size_t i = 0; i < written.size(); ++i)
+    for (size_t i = 0; wstride == 1 && i < written.size(); ++i)
         if (!written[i]) {
             fail("output float %lld never stored", (long long)(i * 4));
             break;

@@ -19,8 +19,9 @@
 //   block  k g_1..g_k B C_in C_mid C_out d_image d_filter path  ACT ACT
 //   act    nb B C P  ACT
 // with ACT = mode K blade_1..blade_K (mode -1: none, K then 0).
-// Output: one line per case, "ok <status> <launches> <checked workgroups>" or
-// "FAIL <message>".
+// Output: one line per case, "ok <status> <launches> <simulated workgroups>
+// <kernel kinds>" (kinds: the LaunchKind of each launch, comma-separated, or
+// "-") or "FAIL <message>".
 #include <inttypes.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -78,8 +79,11 @@ static float* make_buffer(const char* name, int64_t n_floats)
 static void on_launch(const cliff::LaunchPlan& p, void*)
 {
     current->launches++;
+    if (!current->kinds.empty()) current->kinds += ",";
+    current->kinds += std::to_string(p.kind);
     switch (p.kind) {
     case cliff::LAUNCH_CONV_MFMA: check_conv_mfma(p); break;
+    case cliff::LAUNCH_CONV1D_MFMA: check_conv1d(p); break;
     default: check_generic(p); break;
     }
 }
@@ -213,7 +217,8 @@ int main()
         if (c.errors)
             printf("FAIL status %d, %d errors: %s\n", st, c.errors, c.first_error.c_str());
         else
-            printf("ok %d %d %" PRId64 "\n", st, c.launches, c.workgroups);
+            printf("ok %d %d %" PRId64 " %s\n", st, c.launches, c.workgroups,
+                   c.kinds.empty() ? "-" : c.kinds.c_str());
         fflush(stdout);
     }
     cliff::launch_observer = nullptr;

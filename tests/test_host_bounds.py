@@ -9,8 +9,9 @@ the kernel's own address arithmetic over every workgroup and lane.  For the
 matrix-core convolution (k = 2, 3) that is every direct global->LDS load in
 bounds, every LDS word a fragment reads written by the stage with the input
 or filter element the product needs, every output stored once in bounds
-(tests/hostcheck/check_conv_mfma.cpp); the other kernels' launch shapes are
-checked for now.
+(tests/hostcheck/check_conv_mfma.cpp); the same for the 1-D matrix-core
+convolution (check_conv1d.cpp); the other kernels' launch shapes are checked
+for now.
 
 Cases: the GPU parity shapes with every tile shape forced, the benchmark's
 workloads at full size, the random sweeps' draws (convolutions and blocks),
@@ -150,3 +151,16 @@ def test_medium_images_every_tile():
             cases.append(("3D d %d C %d algo %s" % (d, C, ALGO_NAMES[algo]),
                           conv_line(3, (1, 1, 1), 2, C, C, d, 3, algo)))
     _run_cases(cases, _is_forced_tile)
+
+
+def test_wide_images_row_aligned():
+    # 2D images of 2048 and more positions per row: row-aligned blocks only
+    # (whole-row slabs do not fit), 32-bit offsets from the block's rows
+    cases = []
+    for d, C, B in ((2050, 16, 1), (2049, 8, 1), (4098, 4, 1), (3000, 2, 1)):
+        for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_NARROW):
+            cases.append(("2D d %d C %d algo %s" % (d, C, ALGO_NAMES[algo]),
+                          conv_line(2, (1, 1), B, C, C, d, 3, algo)))
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        assert res.split()[4] == "1", (label, res)  # one matrix-core launch, no fallback
