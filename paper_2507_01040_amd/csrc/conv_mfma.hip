@@ -66,6 +66,9 @@
 #ifndef CLIFF_CONV_NEG  // negated filter copy in LDS instead of sign multiplies (wide 3x3(x3) tiles)
 #define CLIFF_CONV_NEG 1
 #endif
+#ifndef CLIFF_CONV_NEG2D  // ... also for the 2D tiles
+#define CLIFF_CONV_NEG2D 0
+#endif
 namespace cliff {
 namespace {
 
@@ -132,9 +135,9 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         }
     };
 
-    // NEG: the stage's filters go through registers (global loads issued
-    // with the stage's direct loads, before its predecessor is multiplied),
-    // then to LDS as they are and negated, after the wait that ends the
+    // NEG: the stage's filters also go through registers (global loads
+    // issued with the stage's direct loads, before its predecessor is
+    // multiplied), then to LDS negated, after the wait that ends the
     // predecessor (the buffer was last read before the previous barrier).
     f4 wreg[FS > 0 ? FS : 1];
     int wsrc[FS > 0 ? FS : 1];
@@ -156,10 +159,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
 #pragma unroll
         for (int u = 0; u < FS; ++u) {
             const int e = u * NT + tid;
-            if (e < cc * wch_f4) {
-                *reinterpret_cast<f4*>(lw + mfma_wreg_lds(g, e, 0)) = wreg[u];
-                *reinterpret_cast<f4*>(lw + mfma_wreg_lds(g, e, 1)) = -wreg[u];
-            }
+            if (e < cc * wch_f4) *reinterpret_cast<f4*>(lw + mfma_wreg_lds(g, e, 1)) = -wreg[u];
         }
     };
 
@@ -426,10 +426,10 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
     const int64_t planes = std::min<int64_t>(R, (R - 1) / Do + 2);
     const int64_t rows_max = R + planes * (df - 1);
     // per channel: LDS floats (slab, filters, NEG: negated filters) and the
-    // floats staged by direct loads (NEG: the slab only)
+    // floats staged by direct loads (slab, filters)
     const int64_t wch = CO_WG * df * df * NB;
     int64_t ch_floats = rows_max * D * NB + (NEG ? 2 : 1) * wch;
-    int64_t ch_dma = rows_max * D * NB + (NEG ? 0 : wch);
+    int64_t ch_dma = rows_max * D * NB + wch;
     // Channels per stage: enough MFMAs per wave between barriers, within the
     // LDS budget (two buffers) and the staging slots.
     constexpr int64_t LDS_BUDGET = LDSKB * 1024;
@@ -458,7 +458,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
                     (cc < 1 && CLIFF_ROWBLK == 1 && p.rowblk == 1))) {
         sw = std::min<int64_t>(P, Do) + df - 1;
         const int64_t chf = df * sw * NB + (NEG ? 2 : 1) * wch;
-        const int64_t chd = df * sw * NB + (NEG ? 0 : wch);
+        const int64_t chd = df * sw * NB + wch;
         const int64_t c = channels(chf, chd);
         if (c >= 1) {
             ch_floats = chf;
@@ -586,9 +586,13 @@ template <int KD, int NB, int DF, int CCT, int WCO, int WPOS, int MW, int NW, in
 cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream,
                            Shape<NB, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB>)
 {
-    // one channel per stage and no zero sign in the table: the negated filter
-    // copy replaces the sign multiplies
-    if constexpr (CCT == 1 && DF > 0 && WK == 1 && CLIFF_CONV_NEG)
+    // 3D, one channel per stage and no zero sign in the table: the negated
+    // filter copy replaces the sign multiplies.  Measured (interleaved, same
+    // box): 3D block layers +1.2-1.3 %, 3D C = 32 +0.1 %; the 2D tiles lose
+    // 1.3-4 % (twice the filter bytes per stage, 2 workgroups per CU: the
+    // copy's LDS writes before the stage barrier cost more than the
+    // multiplies), so they keep the multiplies.
+    if constexpr ((KD == 3 || CLIFF_CONV_NEG2D) && CCT == 1 && DF > 0 && WK == 1 && CLIFF_CONV_NEG)
         if (p.sign.zero == 0)
             return run<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, LDSKB, true>(p,
                                                                                          stream);

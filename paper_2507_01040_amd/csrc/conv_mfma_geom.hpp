@@ -34,9 +34,9 @@ struct MfmaArgs {
 // The compile-time shape of one kernel instantiation, as plain ints: KD
 // spatial dimensions, NB blades, DF filter size (0: run time), CCT channels
 // per stage (0: run time), WCO x WPOS waves of MW x NW MFMA tiles (16 x 16),
-// SLOTS staging slots per lane, the K loop split over WK waves.  NEG: the
-// filters are staged through registers, as they are and negated (two LDS
-// copies), and each A lane reads the copy of its table sign instead of
+// SLOTS staging slots per lane, the K loop split over WK waves.  NEG: LDS
+// also holds the filters negated (loaded again through registers and written
+// negated), and each A lane reads the copy of its table sign instead of
 // multiplying by it (one channel per stage, no zero sign).
 struct MfmaTile {
     int KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WK, NEG;
@@ -45,7 +45,7 @@ struct MfmaTile {
     __host__ __device__ constexpr int co_wg() const { return WCO * MW * (16 / NB); }
     __host__ __device__ constexpr int pos() const { return WPOS * NW * 16; }
     __host__ __device__ constexpr int nh() const { return NB / 4; }  // 4-blade groups
-    // NEG: float4 of filters per lane and stage (filter registers)
+    // NEG: float4 of filters per lane and stage (registers of the negated copy)
     __host__ __device__ constexpr int fslots() const
     {
         return NEG ? (co_wg() * DF * DF * NB / 4 + nt() - 1) / nt() : 0;
@@ -116,8 +116,8 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     g.slab_f4 = g.n_rows * (g.lrow_floats / 4);  // one channel's slab
     g.wq_f4 = g.taps2 * NB / 4;
     g.wch_f4 = T.co_wg() * g.wq_f4;              // one channel's filters
-    // float4 staged by direct loads (NEG: the slabs only)
-    g.total_f4 = g.cc * (g.slab_f4 + (T.NEG ? 0 : g.wch_f4));
+    // float4 staged by direct loads
+    g.total_f4 = g.cc * (g.slab_f4 + g.wch_f4);
     g.w_lds = g.cc * g.slab_f4 * 4;              // float offset of the filters in a buffer
     g.w_neg = g.w_lds + g.cc * g.wch_f4 * 4;     // NEG: of their negated copy
     g.b0 = T.KD == 2 ? g.pl0 : g.pl0 / Do;
@@ -143,8 +143,9 @@ __host__ __device__ inline int mfma_filter_src(const MfmaTile& T, const MfmaArgs
 }
 
 // NEG: filter register slot u of lane tid holds float4 e = u * NT + tid of
-// the stage's filters (when e < cc * wch_f4); it is written to LDS at
-// mfma_wreg_lds(g, e, 0) as it is and at mfma_wreg_lds(g, e, 1) negated.
+// the stage's filters (when e < cc * wch_f4); it is written to LDS negated at
+// mfma_wreg_lds(g, e, 1) (mfma_wreg_lds(g, e, 0) is where the direct loads
+// put it as it is).
 __host__ __device__ inline int mfma_wreg_lds(const MfmaBlock& g, int e, int neg)
 {
     return (neg ? g.w_neg : g.w_lds) + 4 * e;
@@ -152,7 +153,7 @@ __host__ __device__ inline int mfma_wreg_lds(const MfmaBlock& g, int e, int neg)
 
 // Staging.  A stage buffer holds float4 slots in staging order: cc channel
 // slabs [cc][slab rows] in [0, cc * slab_f4), then cc channels of filters
-// [cc][co][tap][blade] (NEG: then their negated copy; the filters do not go
+// [cc][co][tap][blade] (NEG: then their negated copy, which does not go
 // through the direct-load slots but through registers, mfma_wreg_*).  Float4 f = t * NT + tid of the buffer is slot t of
 // lane tid.  Returns its source offset: >= 0, the input float offset from the
 // stage's slab base; < 0, -1 - the filter float offset from the stage's filter

@@ -107,7 +107,7 @@ bool stage_loads(const Ctx& C, const MfmaBlock& g, int s, const std::vector<int>
                 }
             }
         }
-    // NEG: the filters through registers, written as they are and negated
+    // NEG: the filters again through registers, written negated
     for (int u = 0; u < T.fslots(); ++u)
         for (int tid = 0; tid < NT; ++tid) {
             const int e = u * NT + tid;
@@ -119,7 +119,7 @@ bool stage_loads(const Ctx& C, const MfmaBlock& g, int s, const std::vector<int>
                 ok = false;
                 continue;
             }
-            for (int neg = 0; neg < 2; ++neg) {
+            for (int neg = 1; neg < 2; ++neg) {  // the negated copy (the other: direct loads)
                 const int64_t dst = mfma_wreg_lds(g, e, neg);
                 if (dst < 0 || dst + 4 > a.stage_floats ||
                     ((int64_t)buf * a.stage_floats + dst + 4) * 4 > C.lds_bytes) {
