@@ -52,7 +52,9 @@ typedef enum {
     CLIFF_EALIGN = 3,       /* tensor pointer not 16-byte aligned */
     CLIFF_EOVERLAP = 4,     /* output memory overlaps an input */
     CLIFF_EUNSUPPORTED = 5, /* valid request the library does not support */
-    CLIFF_EDEVICE = 6       /* HIP reported an error */
+    CLIFF_EDEVICE = 6,      /* HIP reported an error */
+    CLIFF_ESCRATCH = 7      /* intermediate larger than the library's fixed scratch
+                               (clifford_block2_nd_noalloc only) */
 } cliff_status;
 
 /* Gate aggregation of Algorithm 3. */
@@ -228,6 +230,35 @@ cliff_status clifford_block2_nd_path(int k, const int8_t* g, int64_t B, int64_t 
                                      const float* bias2, const cliff_act_desc* act2,
                                      float* workspace, float* output, void* stream,
                                      int path);
+
+/*
+ * clifford_block2_nd for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same block, without the workspace argument.  A block that
+ * runs as two launches keeps its intermediate in a fixed array inside the
+ * library instead: CLIFF_NOALLOC_SCRATCH_FLOATS fp32 values (64 MiB) of device
+ * memory on every GPU the library has run this call on, held until the
+ * process ends.  The call itself allocates and frees nothing.
+ *   Arguments, layouts, path choice and results: as clifford_block2_nd.
+ *   Limit: B * C_mid * d_mid^k * N_B <= CLIFF_NOALLOC_SCRATCH_FLOATS, else
+ *          CLIFF_ESCRATCH before any work is enqueued (also for blocks that
+ *          would run as one fused launch and need no scratch).
+ *   Sharing: every call on one GPU uses that GPU's one array (its contents are
+ *          whatever the last call left; each call writes every value it
+ *          reads, so nothing needs clearing).  Calls whose executions
+ *          overlap on one GPU -- on different streams, or from several host
+ *          threads without ordering -- race on it and give undefined results.
+ *   Errors: as clifford_block2_nd, plus CLIFF_ESCRATCH, and CLIFF_EDEVICE
+ *          when the array's device address cannot be obtained.
+ */
+#define CLIFF_NOALLOC_SCRATCH_FLOATS (16 * 1024 * 1024)
+cliff_status clifford_block2_nd_noalloc(int k, const int8_t* g, int64_t B, int64_t C_in,
+                                        int64_t C_mid, int64_t C_out, int64_t d_image,
+                                        int64_t d_filter, const float* input,
+                                        const float* filters1, const float* bias1,
+                                        const cliff_act_desc* act1, const float* filters2,
+                                        const float* bias2, const cliff_act_desc* act2,
+                                        float* output, void* stream);
 
 /*
  * Standalone multivector activation (paper, Algorithm 3).

@@ -18,10 +18,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libcliffconv.so")
 
 CLIFF_OK, CLIFF_EINVAL, CLIFF_ESHAPE, CLIFF_EALIGN = 0, 1, 2, 3
-CLIFF_EOVERLAP, CLIFF_EUNSUPPORTED, CLIFF_EDEVICE = 4, 5, 6
+CLIFF_EOVERLAP, CLIFF_EUNSUPPORTED, CLIFF_EDEVICE, CLIFF_ESCRATCH = 4, 5, 6, 7
 STATUS_NAMES = {0: "CLIFF_OK", 1: "CLIFF_EINVAL", 2: "CLIFF_ESHAPE",
                 3: "CLIFF_EALIGN", 4: "CLIFF_EOVERLAP",
-                5: "CLIFF_EUNSUPPORTED", 6: "CLIFF_EDEVICE"}
+                5: "CLIFF_EUNSUPPORTED", 6: "CLIFF_EDEVICE", 7: "CLIFF_ESCRATCH"}
+NOALLOC_SCRATCH_FLOATS = 16 * 1024 * 1024  # CLIFF_NOALLOC_SCRATCH_FLOATS
 AGG_LINEAR, AGG_SUM, AGG_MEAN = 0, 1, 2
 ALGO_AUTO, ALGO_DIRECT, ALGO_MFMA = 0, 1, 2
 ALGO_MFMA_WIDE, ALGO_MFMA_MEDIUM, ALGO_MFMA_NARROW, ALGO_MFMA_TINY = 3, 4, 5, 6
@@ -30,7 +31,8 @@ BLOCK_AUTO, BLOCK_TWO_LAUNCH, BLOCK_FUSED = 0, 1, 2
 
 EXPORTED = ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
             "multivector_act", "cliffconv_cayley_table", "cliffconv_status_string",
-            "cliffconv_mfma_peak_probe", "clifford_block2_nd", "clifford_block2_nd_path")
+            "cliffconv_mfma_peak_probe", "clifford_block2_nd", "clifford_block2_nd_path",
+            "clifford_block2_nd_noalloc")
 
 
 class CliffActDesc(ctypes.Structure):
@@ -73,11 +75,13 @@ def load(path: str = LIB_PATH):
                   ctypes.POINTER(CliffActDesc), vp, vp, ctypes.POINTER(CliffActDesc), vp, vp, vp]
     lib.clifford_block2_nd.argtypes = block_args
     lib.clifford_block2_nd_path.argtypes = block_args + [i32]
+    # the block without the workspace argument
+    lib.clifford_block2_nd_noalloc.argtypes = block_args[:15] + block_args[16:]
     lib.cliffconv_status_string.argtypes = [i32]
     lib.cliffconv_status_string.restype = ctypes.c_char_p
     for name in ("clifford_conv_nd", "clifford_conv_nd_algo", "clifford_linear",
                  "multivector_act", "cliffconv_cayley_table", "cliffconv_mfma_peak_probe",
-                 "clifford_block2_nd", "clifford_block2_nd_path"):
+                 "clifford_block2_nd", "clifford_block2_nd_path", "clifford_block2_nd_noalloc"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -158,6 +162,22 @@ def clifford_block2_nd_path(k: int, g: Sequence[int], B: int, C_in: int, C_mid: 
         ctypes.byref(act1) if act1 is not None else None, filters2_ptr or None,
         bias2_ptr or None, ctypes.byref(act2) if act2 is not None else None,
         workspace_ptr or None, output_ptr or None, stream or None, path)
+
+
+def clifford_block2_nd_noalloc(k: int, g: Sequence[int], B: int, C_in: int, C_mid: int,
+                               C_out: int, d_image: int, d_filter: int, input_ptr: int,
+                               filters1_ptr: int, bias1_ptr: int, act1: Optional[CliffActDesc],
+                               filters2_ptr: int, bias2_ptr: int, act2: Optional[CliffActDesc],
+                               output_ptr: int, stream: int = 0) -> int:
+    """The block without a workspace: the intermediate lives in the library's
+    fixed scratch array (callers that cannot allocate).  Returns the
+    cliff_status."""
+    return load().clifford_block2_nd_noalloc(
+        k, _g_array(g), B, C_in, C_mid, C_out, d_image, d_filter, input_ptr or None,
+        filters1_ptr or None, bias1_ptr or None,
+        ctypes.byref(act1) if act1 is not None else None, filters2_ptr or None,
+        bias2_ptr or None, ctypes.byref(act2) if act2 is not None else None,
+        output_ptr or None, stream or None)
 
 
 def cliffconv_cayley_table(k: int, g: Sequence[int]):

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcliffconv.so")
 SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip",
-           "block_small.hip", "linear_mfma.hip",
+           "block_small.hip", "block_noalloc.hip", "linear_mfma.hip",
            "mfma_probe.hip"]
 ARCH = "gfx950"
 

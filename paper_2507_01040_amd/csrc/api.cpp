@@ -421,6 +421,7 @@ const char* cliffconv_status_string(cliff_status s)
     case CLIFF_EOVERLAP: return "output overlaps an input";
     case CLIFF_EUNSUPPORTED: return "unsupported by the library";
     case CLIFF_EDEVICE: return "HIP device error";
+    case CLIFF_ESCRATCH: return "intermediate exceeds the library's fixed scratch array";
     }
     return "unknown status";
 }

@@ -52,8 +52,8 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings():
     _lib_or_skip()
-    for s in range(7):
-        assert P.status_string(s)
+    for s in range(8):
+        assert P.status_string(s) and "unknown" not in P.status_string(s)
     assert "unknown" in P.status_string(99)
 
 
