@@ -62,14 +62,23 @@ struct LinArgs {
 #ifndef CLIFF_LIN_PF  // chunks of 16 K values prefetched ahead
 #define CLIFF_LIN_PF 4
 #endif
-#ifndef CLIFF_LIN_N64_WAVES4  // N = K = 64: 8 tiles per wave at 4 waves per SIMD
+#ifndef CLIFF_LIN_N64_WAVES4  // N = K = 64: fewer tiles per wave at more waves per SIMD
 #define CLIFF_LIN_N64_WAVES4 1
+#endif
+#ifndef CLIFF_LIN_N64_CHAINS  // ... that many accumulator tiles per wave (one 16-position tile)
+#define CLIFF_LIN_N64_CHAINS 4
+#endif
+#ifndef CLIFF_LIN_N64_WAVES  // ... at that many waves per SIMD
+#define CLIFF_LIN_N64_WAVES 4
 #endif
 #ifndef CLIFF_LIN_NEG  // negated weight copy in LDS instead of sign multiplies
 #define CLIFF_LIN_NEG 1
 #endif
 #ifndef CLIFF_LIN_NEG8  // 8-wave workgroups for 256-column layers whose two copies need them
 #define CLIFF_LIN_NEG8 1
+#endif
+#ifndef CLIFF_LIN_STORE_AUX  // cache policy bits of the output stores
+#define CLIFF_LIN_STORE_AUX 0
 #endif
 #ifndef CLIFF_LIN_WAVES  // waves per SIMD the registers are sized for
 #define CLIFF_LIN_WAVES 2
@@ -271,7 +280,8 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
                     }
                 }
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), ydesc,
-                                                       ((nw * 16 + n) * N + row0) * 4, 0, 0);
+                                                       ((nw * 16 + n) * N + row0) * 4, 0,
+                                                       CLIFF_LIN_STORE_AUX);
             }
         }
         if (!has_next) break;
@@ -303,11 +313,13 @@ template <int NB, int RT, int KQ>
 cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
 {
     // 16 independent accumulator tiles per wave at 2 waves per SIMD; N = K =
-    // 64 (HBM-bound) does better with 8 tiles at 4 waves per SIMD, more loads
-    // in flight (measured +7 % on the 1-D C = 32 layer, -1 to -3 % at N = 128)
+    // 64 (HBM-bound) does better with more waves per SIMD and fewer tiles:
+    // 8 tiles at 4 waves measured +7 % on the 1-D C = 32 layer (-1 to -3 % at
+    // N = 128), 4 tiles (one 16-position tile per wave) at 4 waves a further
+    // +4 % (4.57 -> 4.75 TB/s at B = 2^21; the same at 6 waves per SIMD)
     constexpr bool NARROW_N = RT == 4 && KQ == 4 && CLIFF_LIN_N64_WAVES4;
-    constexpr int CHAINS = NARROW_N ? 8 : CLIFF_LIN_CHAINS;
-    constexpr int WAVES = NARROW_N ? 4 : CLIFF_LIN_WAVES;
+    constexpr int CHAINS = NARROW_N ? CLIFF_LIN_N64_CHAINS : CLIFF_LIN_CHAINS;
+    constexpr int WAVES = NARROW_N ? CLIFF_LIN_N64_WAVES : CLIFF_LIN_WAVES;
     constexpr int NWW = RT >= CHAINS ? 1 : CHAINS / RT;
     // (N = 64 with K = 256: 2 chunks, which keeps that unrolled kernel
     // within the registers of 2 waves per SIMD)
