@@ -84,20 +84,32 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
               S2 = ipow_dev(a.D2, KD - 1);
 
     // 1. Stage the input band ([C0][R0][S0][NB], slices s0.. of each channel
-    //    are contiguous in HBM) and both layers' raw filters.
+    //    are contiguous in HBM) and both layers' raw filters, by direct
+    //    global->LDS loads: float4 e of each array goes to LDS float4 e of its
+    //    area, so a wave's 64 loads fill 1 KB from the wave's first float4 on.
+    //    All of them are issued before the one wait (a load-to-register loop
+    //    waits for each load before the next).
     {
+        const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+        auto dma = [&](const float* src, int lds_f4) {
+            __builtin_amdgcn_global_load_lds(
+                src, (__attribute__((address_space(3))) void*)(smem + 4 * lds_f4), 16, 0, 0);
+        };
         const int ch4 = R0 * S0 * NB / 4;
-        const f4* xg = reinterpret_cast<const f4*>(a.x);
-        for (int e = tid; e < a.C0 * ch4; e += BS_THREADS) {
-            const int ci = e / ch4;
-            const int r = e - ci * ch4;
-            smem4[e] = xg[(((int64_t)b * a.C0 + ci) * a.D0 + s0) * S0 * NB / 4 + r];
+        for (int e0 = wave_u * 64; e0 < a.C0 * ch4; e0 += BS_THREADS) {
+            const int e = e0 + lane;
+            if (e < a.C0 * ch4) {
+                const int ci = e / ch4;
+                const int r = e - ci * ch4;
+                dma(a.x + ((((int64_t)b * a.C0 + ci) * a.D0 + s0) * S0 * NB + 4 * r), e0);
+            }
         }
         const int n1 = a.C0 * a.C1 * taps * NB / 4, n2 = a.C1 * a.C2 * taps * NB / 4;
-        const f4* w1 = reinterpret_cast<const f4*>(a.w1);
-        const f4* w2 = reinterpret_cast<const f4*>(a.w2);
-        for (int e = tid; e < n1; e += BS_THREADS) smem4[a.lds_w1 / 4 + e] = w1[e];
-        for (int e = tid; e < n2; e += BS_THREADS) smem4[a.lds_w2 / 4 + e] = w2[e];
+        for (int e0 = wave_u * 64; e0 < n1; e0 += BS_THREADS)
+            if (e0 + lane < n1) dma(a.w1 + 4 * (e0 + lane), a.lds_w1 / 4 + e0);
+        for (int e0 = wave_u * 64; e0 < n2; e0 += BS_THREADS)
+            if (e0 + lane < n2) dma(a.w2 + 4 * (e0 + lane), a.lds_w2 / 4 + e0);
+        __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
     __syncthreads();
 
@@ -137,6 +149,21 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             const int yy = KD == 3 ? r / dout : 0, xx = KD == 3 ? r - yy * dout : r;
             const float* wrow = w + co_r * taps * NB;
             const float* xcol = in + (so * Sin + yy * din + xx) * NB + kk;
+            // The epilogue's parameters, loaded before the MFMAs so that the
+            // loads run during them.  The loads are unconditional (an absent
+            // parameter reads the input's first floats instead, and the value
+            // is not used): loads under a condition would be moved into the
+            // epilogue, behind the last MFMA.
+            const int co = rt * CPT + co_o;
+            const bool cvalid = co < Cout;
+            const int co_c = min(co, Cout - 1);
+            const bool lin = act.mode == CLIFF_AGG_LINEAR;
+            const f4 bv = *reinterpret_cast<const f4*>(bias ? bias + co_c * NB + i0 : a.x);
+            float gw[4];
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2)
+                gw[r2] = *(lin ? act.weight + (int64_t)co_c * act.K + max(gslot[r2], 0) : a.x);
+            const float gb = *(lin ? act.bias + co_c : a.x);
             // BS_ACC partial sums over the K steps (independent MFMA chains),
             // added at the end
             f4 acc[BS_ACC];
@@ -181,19 +208,20 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             f4 v = acc[0];
 #pragma unroll
             for (int q = 1; q < BS_ACC; ++q) v += acc[q];
-            // epilogue: bias, activation (gate over the channel's N_B blades)
-            const int co = rt * CPT + co_o;
-            const bool cvalid = co < Cout;
+            // epilogue: bias, activation (gate over the channel's N_B blades;
+            // gate_coef's weights: the Linear gate's, 1 for Sum and Mean, 0
+            // outside the subset)
             const int m = pt * 16 + mrow;
-            if (cvalid && bias) v += *reinterpret_cast<const f4*>(bias + co * NB + i0);
+            if (cvalid && bias) v += bv;
             if (has_act) {
                 float part = 0.f;
                 if (cvalid) {
 #pragma unroll
-                    for (int r2 = 0; r2 < 4; ++r2) part += gate_coef(act, gslot[r2], co) * v[r2];
+                    for (int r2 = 0; r2 < 4; ++r2)
+                        part += (gslot[r2] < 0 ? 0.f : lin ? gw[r2] : 1.f) * v[r2];
                 }
                 if (NB == 8) part += __shfl_xor(part, 16);
-                const float gate = cvalid ? gate_sigmoid(act, part, co) : 0.f;
+                const float gate = cvalid ? gate_from_sum(act, part, gb) : 0.f;
                 v *= gate;
             }
             if (cvalid && m < npos) store(co, m, v);

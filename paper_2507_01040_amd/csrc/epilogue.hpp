@@ -25,16 +25,22 @@ __device__ inline float gate_coef(const ActParams& act, int slot, int c)
                                         : 1.0f;
 }
 
-// Gate value s from the full aggregated sum (Linear adds the channel bias,
-// Mean divides by K), then sigmoid(s) = 1 / (1 + exp(-s)).
-__device__ inline float gate_sigmoid(const ActParams& act, float sum, int c)
+// Gate value s from the full aggregated sum (Linear adds the channel's bias
+// `lin_bias`, Mean divides by K), then sigmoid(s) = 1 / (1 + exp(-s)).
+__device__ inline float gate_from_sum(const ActParams& act, float sum, float lin_bias)
 {
     float s = sum;
     if (act.mode == CLIFF_AGG_LINEAR)
-        s = s + act.bias[c];
+        s = s + lin_bias;
     else if (act.mode == CLIFF_AGG_MEAN)
         s = s / (float)act.K;
     return 1.0f / (1.0f + __expf(-s));
+}
+
+// The same for channel c, its Linear bias read from the descriptor.
+__device__ inline float gate_sigmoid(const ActParams& act, float sum, int c)
+{
+    return gate_from_sum(act, sum, act.mode == CLIFF_AGG_LINEAR ? act.bias[c] : 0.0f);
 }
 
 }  // namespace cliff
