@@ -321,6 +321,40 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
       }
     };
 
+    // D fragment: lane holds output channel co and blades i0..i0+3 of one
+    // position; gslot[r] is blade i0 + r's place in the gate's blade list.
+    const int i0 = mfma_out_blade0(TL, L);
+    const bool has_act = a.act.mode >= 0;
+    const bool lin = a.act.mode == CLIFF_AGG_LINEAR;
+    // Tiles with a split K loop (the smallest problems, bound by latency)
+    // load the epilogue's parameters before the main loop, unconditionally
+    // (an absent parameter reads the input's first floats, unused), so that
+    // the loads run under the MFMAs: issued after the loop, each round trip
+    // would follow the last MFMA, and under a condition the compiler moves
+    // them there.  The other tiles load them in the epilogue, where their
+    // registers are free.
+    constexpr bool EARLY = WK > 1;
+    constexpr int ME = EARLY ? MW : 1;
+    int gslot[4] = {-1, -1, -1, -1};
+    f4 ebb[ME];
+    float ecf[ME][4], egb[ME];
+    if constexpr (EARLY) {
+        if (has_act) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) gslot[r] = gate_slot(a.act, i0 + r);
+        }
+#pragma unroll
+        for (int mw = 0; mw < MW; ++mw) {
+            const int co_c = min(mfma_out_channel(TL, g, L, mw), a.C_out - 1);
+            ebb[mw] = *reinterpret_cast<const f4*>(a.bias ? a.bias + co_c * NB + i0 : a.x);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                ecf[mw][r] = *(lin ? a.act.weight + (int64_t)co_c * a.act.K + max(gslot[r], 0)
+                                   : a.x);
+            egb[mw] = *(lin ? a.act.bias + co_c : a.x);
+        }
+    }
+
     // Main loop: one barrier per stage; the next stage's global loads are in
     // flight while the current one is multiplied.
     load_stage(0, 0);
@@ -364,25 +398,31 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     }
 
     // Epilogue: bias, optional multivector activation, 16-byte stores.
-    // D fragment: lane holds output channel co and blades i0..i0+3 of one
-    // position.
-    const int i0 = mfma_out_blade0(TL, L);
-    const bool has_act = a.act.mode >= 0;
-    int gslot[4] = {-1, -1, -1, -1};
-    if (has_act) {
+    if constexpr (!EARLY) {
+        if (has_act) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) gslot[r] = gate_slot(a.act, i0 + r);
+            for (int r = 0; r < 4; ++r) gslot[r] = gate_slot(a.act, i0 + r);
+        }
     }
 #pragma unroll
     for (int mw = 0; mw < MW; ++mw) {
         const int co = mfma_out_channel(TL, g, L, mw);
         const bool cvalid = co < a.C_out;
         f4 bb = f4{0.f, 0.f, 0.f, 0.f};
-        if (cvalid && a.bias) bb = *reinterpret_cast<const f4*>(a.bias + co * NB + i0);
         float cf[4] = {0.f, 0.f, 0.f, 0.f};
-        if (has_act && cvalid) {
+        if constexpr (EARLY) {
+            // gate_coef's weights from the loaded values
+            if (cvalid && a.bias) bb = ebb[mw];
+            if (has_act && cvalid) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) cf[r] = gate_coef(a.act, gslot[r], co);
+                for (int r = 0; r < 4; ++r) cf[r] = gslot[r] < 0 ? 0.f : lin ? ecf[mw][r] : 1.f;
+            }
+        } else {
+            if (cvalid && a.bias) bb = *reinterpret_cast<const f4*>(a.bias + co * NB + i0);
+            if (has_act && cvalid) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) cf[r] = gate_coef(a.act, gslot[r], co);
+            }
         }
 #pragma unroll
         for (int nw = 0; nw < NW; ++nw) {
@@ -391,7 +431,9 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
             if (has_act) {
                 float part = cf[0] * v[0] + cf[1] * v[1] + cf[2] * v[2] + cf[3] * v[3];
                 if (NB == 8) part += __shfl_xor(part, 16);
-                const float gate = cvalid ? gate_sigmoid(a.act, part, co) : 0.f;
+                float gate = 0.f;
+                if (cvalid)
+                    gate = EARLY ? gate_from_sum(a.act, part, egb[mw]) : gate_sigmoid(a.act, part, co);
                 v *= gate;
             }
             if (cvalid && m < m_end)
