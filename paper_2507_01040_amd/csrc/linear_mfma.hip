@@ -77,6 +77,9 @@ struct LinArgs {
 #ifndef CLIFF_LIN_NEG8  // 8-wave workgroups for 256-column layers whose two copies need them
 #define CLIFF_LIN_NEG8 1
 #endif
+#ifndef CLIFF_LIN_AREG  // N = K = 64: the signed A values in registers for the whole kernel
+#define CLIFF_LIN_AREG 1
+#endif
 #ifndef CLIFF_LIN_STORE_AUX  // cache policy bits of the output stores
 #define CLIFF_LIN_STORE_AUX 0
 #endif
@@ -160,6 +163,20 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
     float fa[2][RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) fa[0][rt] = wl[abase[0] + 16 * rt];
+    // N = K = 64: every step's signed A values stay in registers (64 per
+    // lane), read and signed once, so the tile loop has no LDS reads and no
+    // multiplies
+    constexpr bool AREG = CLIFF_LIN_AREG && RT * 4 * KQ <= 64;
+    float areg[AREG ? 4 * KQ : 1][RT];
+    if constexpr (AREG) {
+#pragma unroll
+        for (int s = 0; s < 4 * KQ; ++s)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const float w = wl[abase[s % 4] + (s / 4) * QS + 16 * rt];
+                areg[s][rt] = NEG ? w : w * sg[s % 4];
+            }
+    }
 
     // One tile's K loop, fully unrolled (KQ is a compile-time constant), so
     // that the compiler's wait counts stay exact: at a loop header it would
@@ -185,12 +202,18 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
             // (step 0 of the next tile after the last) spread between this
             // step's MFMAs, so their LDS latency is hidden
             float as[RT];
+            if constexpr (AREG) {
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) as[rt] = NEG ? fa[cur][rt] : fa[cur][rt] * sg[st];
-            const int s1 = (s + 1) % (4 * KQ);
+                for (int rt = 0; rt < RT; ++rt) as[rt] = areg[s][rt];
+            } else {
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-                fa[cur ^ 1][rt] = wl[abase[s1 % 4] + (s1 / 4) * QS + 16 * rt];
+                for (int rt = 0; rt < RT; ++rt)
+                    as[rt] = NEG ? fa[cur][rt] : fa[cur][rt] * sg[st];
+                const int s1 = (s + 1) % (4 * KQ);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    fa[cur ^ 1][rt] = wl[abase[s1 % 4] + (s1 / 4) * QS + 16 * rt];
+            }
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -208,11 +231,13 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
                     ring[p][nw] = *reinterpret_cast<const f4*>(src);
                 }
             }
-            if (!NEG) __builtin_amdgcn_sched_group_barrier(0x002, RT, 0);  // sign multiplies
+            if constexpr (!AREG) {
+                if (!NEG) __builtin_amdgcn_sched_group_barrier(0x002, RT, 0);  // sign multiplies
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                __builtin_amdgcn_sched_group_barrier(0x008, NWW, 0);  // MFMA
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
+                for (int rt = 0; rt < RT; ++rt) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, NWW, 0);  // MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
+                }
             }
             __builtin_amdgcn_sched_group_barrier(0x008, RT * NWW, 0);
             __builtin_amdgcn_sched_group_barrier(0x020, NWW, 0);      // global loads
