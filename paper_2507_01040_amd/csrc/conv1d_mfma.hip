@@ -386,7 +386,9 @@ cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
 
 // Tile shapes (waves along channels x waves along positions, MFMA tiles per
 // wave along channels x along positions):
-//   wide   2x2 waves of 4x4 tiles: 64 channels x 128 positions
+//   wide   2x2 waves of 4x4 tiles: 64 channels x 128 positions (d_filter 17:
+//          also 4x1 waves of 2x11 tiles, 64 channels x 176 positions, where
+//          its blocks fill the last round of CUs better)
 //   medium 2x1 waves of 4x2 tiles: 64 channels x  32 positions
 //   narrow 1x4 waves of 1x4 tiles:  8 channels x 256 positions
 //   tiny   1x2 tiles:                8 channels x  32 positions (long K loops
@@ -398,6 +400,12 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     // 16-byte loads, waves per SIMD>
     auto wide = [&] {
         return run1d_fw<DF, CLIFF_W1, 18, 6, DF == 17 ? CLIFF_W1_WAVES17 : CLIFF_W1_WAVES>(p, stream);
+    };
+    // the 176-position form: 4x1 waves of 2x11 tiles, 2 waves per SIMD (at
+    // 3 it spills registers)
+    auto wide176 = [&] {
+        if constexpr (DF == 17) return run1d_fw<DF, 4, 1, 2, 11, 8, 18, 6, 2>(p, stream);
+        return CLIFF_EUNSUPPORTED;
     };
     auto medium = [&] { return run1d_fw<DF, 2, 1, 4, 2, 8, 18, 9, 2>(p, stream); };
     auto narrow = [&] { return run1d_fw<DF, 1, 4, 1, 4, 16, 4, 2, 2>(p, stream); };
@@ -411,13 +419,6 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
             return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4, 4>(p, stream);
         return run1d_fw<DF, 1, 1, 1, 2, 12, 12, 4, 4, 1>(p, stream);
     };
-    switch (p.mfma_shape) {
-    case 0: return wide();
-    case 1: return medium();
-    case 2: return narrow();
-    case 3: return tiny();
-    default: break;
-    }
     const int64_t M = p.B * p.d_out;
     auto blocks = [&](int64_t co_wg, int64_t pos) {
         return ((M + pos - 1) / pos) * ((p.C_out + co_wg - 1) / co_wg);
@@ -429,18 +430,35 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
     // 0.68 (tiny).  Smaller layers keep the latency rule below.
     const double useful = 2.0 * M * p.C_out * 2 * p.C_in * 2 * p.d_filter;
     const int cus = device_cus();
-    if (CLIFF_SHAPE_MODEL1 && useful >= 1e9 && cus > 0) {
-        auto est = [&](int64_t co_wg, int64_t pos, double b) {
-            const int64_t n = blocks(co_wg, pos);
-            const int64_t rounds = (n + cus - 1) / cus;
-            const double u =
-                (double)p.C_out / (double)(((p.C_out + co_wg - 1) / co_wg) * co_wg);
-            return b * (double)n / (double)(rounds * cus) * u;
-        };
-        const double ew = p.C_out > 32 ? est(64, 128, 0.90) : 0.0;
+    const bool model = CLIFF_SHAPE_MODEL1 && useful >= 1e9 && cus > 0;
+    auto est = [&](int64_t co_wg, int64_t pos, double b) {
+        const int64_t n = blocks(co_wg, pos);
+        const int64_t rounds = (n + cus - 1) / cus;
+        const double u = (double)p.C_out / (double)(((p.C_out + co_wg - 1) / co_wg) * co_wg);
+        return b * (double)n / (double)(rounds * cus) * u;
+    };
+    // the wide tile's width: 176 positions where the model rates it higher
+    // (b = 0.89 against 0.90, fitted like the others)
+    auto wide_best = [&] {
+        cliff_status s = CLIFF_EUNSUPPORTED;
+        if (model && DF == 17 && est(64, 176, 0.89) > est(64, 128, 0.90)) s = wide176();
+        if (s == CLIFF_EUNSUPPORTED) s = wide();
+        return s;
+    };
+    switch (p.mfma_shape) {
+    case 0: return wide_best();
+    case 1: return medium();
+    case 2: return narrow();
+    case 3: return tiny();
+    default: break;
+    }
+    if (model) {
+        const double ew =
+            p.C_out > 32 ? std::max(est(64, 128, 0.90), DF == 17 ? est(64, 176, 0.89) : 0.0)
+                         : 0.0;
         const double en = est(8, 256, 0.80), et = est(8, 32, 0.68);
         cliff_status s = CLIFF_EUNSUPPORTED;
-        if (ew >= en && ew >= et) s = wide();
+        if (ew >= en && ew >= et) s = wide_best();
         if (s == CLIFF_EUNSUPPORTED && en >= et) s = narrow();
         if (s == CLIFF_EUNSUPPORTED) s = tiny();
         if (s == CLIFF_EUNSUPPORTED) s = narrow();

@@ -30,6 +30,7 @@ struct Case {
     int64_t workgroups = 0;  // workgroups whose LDS image was simulated
     bool grid_sampled = false;  // a grid too large to walk every workgroup
     std::string kinds;          // LaunchKind of each launch, comma-separated
+    std::string tiles;          // each launch's template values, '.'-joined, comma-separated
     int errors = 0;
     std::string first_error;
 };

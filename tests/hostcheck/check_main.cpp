@@ -20,8 +20,9 @@
 //   act    nb B C P  ACT
 // with ACT = mode K blade_1..blade_K (mode -1: none, K then 0).
 // Output: one line per case, "ok <status> <launches> <simulated workgroups>
-// <kernel kinds>" (kinds: the LaunchKind of each launch, comma-separated, or
-// "-") or "FAIL <message>".
+// <kernel kinds> <tiles>" (kinds: the LaunchKind of each launch,
+// comma-separated, or "-"; tiles: each launch's template arguments joined by
+// '.', comma-separated, or "-") or "FAIL <message>".
 #include <inttypes.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -81,6 +82,8 @@ static void on_launch(const cliff::LaunchPlan& p, void*)
     current->launches++;
     if (!current->kinds.empty()) current->kinds += ",";
     current->kinds += std::to_string(p.kind);
+    if (!current->tiles.empty()) current->tiles += ",";
+    for (int t = 0; t < 12; ++t) current->tiles += (t ? "." : "") + std::to_string(p.tpl[t]);
     switch (p.kind) {
     case cliff::LAUNCH_CONV_MFMA: check_conv_mfma(p); break;
     case cliff::LAUNCH_CONV1D_MFMA: check_conv1d(p); break;
@@ -217,8 +220,9 @@ int main()
         if (c.errors)
             printf("FAIL status %d, %d errors: %s\n", st, c.errors, c.first_error.c_str());
         else
-            printf("ok %d %d %" PRId64 " %s\n", st, c.launches, c.workgroups,
-                   c.kinds.empty() ? "-" : c.kinds.c_str());
+            printf("ok %d %d %" PRId64 " %s %s\n", st, c.launches, c.workgroups,
+                   c.kinds.empty() ? "-" : c.kinds.c_str(),
+                   c.tiles.empty() ? "-" : c.tiles.c_str());
         fflush(stdout);
     }
     cliff::launch_observer = nullptr;
