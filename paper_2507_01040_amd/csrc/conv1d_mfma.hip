@@ -371,8 +371,9 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
 
 // 16-byte filter loads (fewer slots) when C_out is even, and then also
 // 16-byte input loads when d_image is even; 4-byte loads otherwise.
+// (FW1: the shape has a 4-byte filter form at all)
 template <int DF, int WCO, int WPOS, int MW, int NW, int SIN, int SW1, int SW4, int WAVES,
-          int WK = 1>
+          int WK = 1, bool FW1 = true>
 cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
 {
     constexpr int SIN4 = (SIN + 3) / 4 + 1;  // 16-byte input slots (one more position)
@@ -381,7 +382,10 @@ cliff_status run1d_fw(const ConvProblem& p, hipStream_t stream)
     if (p.C_out % 2 == 0)
         return run1d<DF, WCO, WPOS, MW, NW, SIN, SW4, WAVES, 4, 1, WK>(p, stream);
     // (the 4-byte filter slots need more registers: at most 2 waves per SIMD)
-    return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, (WAVES < 2 ? WAVES : 2), 1, 1, WK>(p, stream);
+    if constexpr (FW1)
+        return run1d<DF, WCO, WPOS, MW, NW, SIN, SW1, (WAVES < 2 ? WAVES : 2), 1, 1, WK>(p,
+                                                                                       stream);
+    return CLIFF_EUNSUPPORTED;
 }
 
 // Tile shapes (waves along channels x waves along positions, MFMA tiles per
@@ -402,9 +406,10 @@ cliff_status run1d_shape(const ConvProblem& p, hipStream_t stream)
         return run1d_fw<DF, CLIFF_W1, 18, 6, DF == 17 ? CLIFF_W1_WAVES17 : CLIFF_W1_WAVES>(p, stream);
     };
     // the 176-position form: 4x1 waves of 2x11 tiles, 2 waves per SIMD (at
-    // 3 it spills registers)
+    // 3 it spills registers, and so do its 4-byte filter slots: even C_out
+    // only)
     auto wide176 = [&] {
-        if constexpr (DF == 17) return run1d_fw<DF, 4, 1, 2, 11, 8, 18, 6, 2>(p, stream);
+        if constexpr (DF == 17) return run1d_fw<DF, 4, 1, 2, 11, 8, 18, 6, 2, 1, false>(p, stream);
         return CLIFF_EUNSUPPORTED;
     };
     auto medium = [&] { return run1d_fw<DF, 2, 1, 4, 2, 8, 18, 9, 2>(p, stream); };

@@ -170,12 +170,14 @@ def test_conv1d_176_position_tile():
     # The paper's 1-D filter length (17) on layers whose blocks fill the last
     # round of CUs better at 176 positions than at 128: the quantisation
     # model takes the 176-position form of the wide tile (template NW = 11),
-    # and the checker walks it, with 16-byte (even C_out) and 4-byte (odd)
-    # filter loads.  At B = 8192 the 128-position form fills every round.
+    # and the checker walks it, with 16-byte (d_image even) and 4-byte (odd)
+    # input loads.  At B = 8192 the 128-position form fills every round; odd
+    # C_out (4-byte filter loads) keeps it too.
     cases, want = [], []
     for B, C_in, C_out, d, nw in ((4096, 64, 64, 60, 11), (1024, 64, 64, 60, 11),
-                                  (1000, 64, 63, 60, 11), (2048, 128, 128, 60, 11),
-                                  (1001, 64, 64, 61, 11), (8192, 64, 64, 60, 4)):
+                                  (1000, 64, 62, 60, 11), (2048, 128, 128, 60, 11),
+                                  (1001, 64, 64, 61, 11), (8192, 64, 64, 60, 4),
+                                  (1000, 64, 63, 60, 4)):
         for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE):
             cases.append(("1-D B %d C %d->%d d %d algo %s" % (B, C_in, C_out, d, ALGO_NAMES[algo]),
                           conv_line(1, (-1,), B, C_in, C_out, d, 17, algo)))
