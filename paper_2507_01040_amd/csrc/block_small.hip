@@ -24,6 +24,7 @@
 
 #include <algorithm>
 
+#include "block_small_geom.hpp"
 #include "common.hpp"
 #include "epilogue.hpp"
 
@@ -35,34 +36,9 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 constexpr int BS_THREADS = 256;
 constexpr int BS_ACC = 4;  // independent accumulator chains per wave
 
-struct BlockArgs {
-    const float* x;
-    const float* w1;
-    const float* b1;
-    const float* w2;
-    const float* b2;
-    float* y;
-    int C0, C1, C2;   // input, intermediate and output channels
-    int D0, D1, D2;   // their spatial sizes
-    int df, taps;     // d_filter and d_filter^k
-    int R;            // final-output slices per workgroup
-    int n_band;       // bands per batch entry
-    int lds_y1, lds_w1, lds_w2;  // float offsets in LDS (the input band is at 0)
-    SignMasks sign;
-    ActParams act1, act2;
-};
-
-__device__ inline int ipow_dev(int a, int k)
-{
-    int r = 1;
-    for (int t = 0; t < k; ++t) r *= a;
-    return r;
-}
-
 template <int KD, int NB, int DF>
 __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
 {
-    constexpr int CPT = 16 / NB;  // output channels per 16-row tile
     constexpr int NH = NB / 4;    // K-groups of 4 input blades
     // taps of one input slice handled together: all of them when d_filter is
     // a compile-time constant, else BS_ACC at a time
@@ -75,13 +51,8 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     constexpr int NWAVE = BS_THREADS / 64;
-    const int b = blockIdx.x / a.n_band;
-    const int s0 = (blockIdx.x - b * a.n_band) * a.R;
-    const int R2 = min(a.R, a.D2 - s0);
-    const int R1 = R2 + df - 1;
-    const int R0 = R1 + df - 1;
-    const int S0 = ipow_dev(a.D0, KD - 1), S1 = ipow_dev(a.D1, KD - 1),
-              S2 = ipow_dev(a.D2, KD - 1);
+    // band, layer, lane and tile geometry: block_small_geom.hpp
+    const BsBand g = bs_band(a, KD, df, blockIdx.x);
 
     // 1. Stage the input band ([C0][R0][S0][NB], slices s0.. of each channel
     //    are contiguous in HBM) and both layers' raw filters, by direct
@@ -95,15 +66,9 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             __builtin_amdgcn_global_load_lds(
                 src, (__attribute__((address_space(3))) void*)(smem + 4 * lds_f4), 16, 0, 0);
         };
-        const int ch4 = R0 * S0 * NB / 4;
-        for (int e0 = wave_u * 64; e0 < a.C0 * ch4; e0 += BS_THREADS) {
-            const int e = e0 + lane;
-            if (e < a.C0 * ch4) {
-                const int ci = e / ch4;
-                const int r = e - ci * ch4;
-                dma(a.x + ((((int64_t)b * a.C0 + ci) * a.D0 + s0) * S0 * NB + 4 * r), e0);
-            }
-        }
+        const int nx = a.C0 * bs_band_f4(g, NB);
+        for (int e0 = wave_u * 64; e0 < nx; e0 += BS_THREADS)
+            if (e0 + lane < nx) dma(a.x + bs_band_src(a, g, NB, e0 + lane), e0);
         const int n1 = a.C0 * a.C1 * taps * NB / 4, n2 = a.C1 * a.C2 * taps * NB / 4;
         for (int e0 = wave_u * 64; e0 < n1; e0 += BS_THREADS)
             if (e0 + lane < n1) dma(a.w1 + 4 * (e0 + lane), a.lds_w1 / 4 + e0);
@@ -113,28 +78,24 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
     }
     __syncthreads();
 
-    const int mrow = lane & 15;
-    const int kk = lane >> 4;
-    const int co_a = mrow / NB, i_a = mrow % NB;  // A row
+    const BsLane ln = bs_lane(NB, lane);
+    const int i0 = ln.i0;
     float sg[NH];
     int srcb[NH];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-        sg[h] = sign_of(a.sign, i_a * NB + 4 * h + kk);
-        srcb[h] = src_blade(NB, i_a, 4 * h + kk);
+        sg[h] = sign_of(a.sign, ln.i_a * NB + 4 * h + ln.kk);
+        srcb[h] = src_blade(NB, ln.i_a, 4 * h + ln.kk);
     }
-    // D fragment: rows 4 kk + r = channel co_o of the tile, blades i0..i0+3
-    const int co_o = NB == 4 ? kk : (kk >> 1);
-    const int i0 = NB == 4 ? 0 : 4 * (kk & 1);
 
-    // One layer: input [Cin][Rin][Sin][NB] in LDS (spatial size din), output
-    // Rout x Sout positions of Cout channels; `store(co, m, v)` writes one
-    // lane's 4 blades.
-    auto layer = [&](const float* in, int Cin, int Rin, int din, int Sin, const float* w,
-                     int Cout, int Rout, int dout, int Sout, const float* bias,
+    // One layer (BsLayer: input [Cin][Rin][Sin][NB] in LDS at `in`, filters
+    // at `w`, Rout x Sout output positions of Cout channels); `store(co, m,
+    // v)` writes one lane's 4 blades.
+    auto layer = [&](const float* in, const float* w, const BsLayer& L, const float* bias,
                      const ActParams& act, auto store) {
-        const int npos = Rout * Sout;
-        const int PT = (npos + 15) / 16, RT = (Cout + CPT - 1) / CPT, T = PT * RT;
+        const int Cin = L.Cin, Cout = L.Cout;
+        const int npos = L.Rout * L.Sout;
+        const int T = bs_tiles(L, NB);
         const bool has_act = act.mode >= 0;
         int gslot[4] = {-1, -1, -1, -1};
         if (has_act) {
@@ -142,19 +103,13 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             for (int r = 0; r < 4; ++r) gslot[r] = gate_slot(act, i0 + r);
         }
         for (int t = wave; t < T; t += NWAVE) {  // wave-uniform tile loop
-            const int rt = t % RT, pt = t / RT;
-            const int co_r = min(rt * CPT + co_a, Cout - 1);  // A row (clamped)
-            const int m_r = min(pt * 16 + mrow, npos - 1);     // B column (clamped)
-            const int so = m_r / Sout, r = m_r - so * Sout;
-            const int yy = KD == 3 ? r / dout : 0, xx = KD == 3 ? r - yy * dout : r;
-            const float* wrow = w + co_r * taps * NB;
-            const float* xcol = in + (so * Sin + yy * din + xx) * NB + kk;
+            const BsTile tl = bs_tile(L, KD, NB, taps, ln, t);
             // The epilogue's parameters, loaded before the MFMAs so that the
             // loads run during them.  The loads are unconditional (an absent
             // parameter reads the input's first floats instead, and the value
             // is not used): loads under a condition would be moved into the
             // epilogue, behind the last MFMA.
-            const int co = rt * CPT + co_o;
+            const int co = tl.co;
             const bool cvalid = co < Cout;
             const int co_c = min(co, Cout - 1);
             const bool lin = act.mode == CLIFF_AGG_LINEAR;
@@ -171,8 +126,8 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             for (int q = 0; q < BS_ACC; ++q) acc[q] = f4{0.f, 0.f, 0.f, 0.f};
             const int nrt = KD == 3 ? df * df : df;  // taps per input slice
             for (int ci = 0; ci < Cin; ++ci) {
-                const float* wc = wrow + ci * Cout * taps * NB;
-                const float* xc = xcol + ci * Rin * Sin * NB;
+                const float* wc = w + bs_a_ci(L, tl, NB, taps, ci);
+                const float* xc = in + bs_b_ci(L, tl, NB, ci);
 #pragma unroll
                 for (int qs = 0; qs < (DF > 0 ? DF : 1); ++qs) {
                     for (int qsr = 0; qsr < (DF > 0 ? 1 : df); ++qsr) {
@@ -188,11 +143,18 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
                                 const int qy = KD == 3 ? u / df : 0;
                                 const int qx = KD == 3 ? u - qy * df : u;
                                 const int tap = qs_ * nrt + u;
-                                const int toff = (qs_ * Sin + qy * din + qx) * NB;
 #pragma unroll
                                 for (int h = 0; h < NH; ++h) {
-                                    av[q * NH + h] = wc[tap * NB + srcb[h]] * sg[h];
-                                    bv[q * NH + h] = xc[toff + 4 * h];
+                                    // (2D: whole offsets per read, measured 4-9 %
+                                    // faster; 3D: the channel bases, 1-2 %)
+                                    if constexpr (KD == 2) {
+                                        av[q * NH + h] =
+                                            w[bs_a_ofs(L, tl, NB, taps, ci, tap, srcb[h])] * sg[h];
+                                        bv[q * NH + h] = in[bs_b_ofs(L, tl, NB, ci, qs_, qy, qx, h)];
+                                    } else {
+                                        av[q * NH + h] = wc[bs_a_tap(NB, tap, srcb[h])] * sg[h];
+                                        bv[q * NH + h] = xc[bs_b_tap(L, NB, qs_, qy, qx, h)];
+                                    }
                                 }
                             }
 #pragma unroll
@@ -211,7 +173,7 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             // epilogue: bias, activation (gate over the channel's N_B blades;
             // gate_coef's weights: the Linear gate's, 1 for Sum and Mean, 0
             // outside the subset)
-            const int m = pt * 16 + mrow;
+            const int m = tl.m;
             if (cvalid && bias) v += bv;
             if (has_act) {
                 float part = 0.f;
@@ -230,17 +192,14 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
 
     // 2. First layer: input band -> intermediate band [C1][R1][S1][NB] in LDS.
     float* y1 = smem + a.lds_y1;
-    layer(smem, a.C0, R0, a.D0, S0, smem + a.lds_w1, a.C1, R1, a.D1, S1, a.b1, a.act1,
-          [&](int co, int m, f4 v) {
-              *reinterpret_cast<f4*>(y1 + ((int64_t)co * R1 * S1 + m) * NB + i0) = v;
-          });
+    layer(smem, smem + a.lds_w1, bs_layer1(a, g), a.b1, a.act1, [&](int co, int m, f4 v) {
+        *reinterpret_cast<f4*>(y1 + bs_y1_ofs(g, NB, co, m, i0)) = v;
+    });
     __syncthreads();
     // 3. Second layer: intermediate band -> output slices s0..s0+R2 in HBM.
-    layer(y1, a.C1, R1, a.D1, S1, smem + a.lds_w2, a.C2, R2, a.D2, S2, a.b2, a.act2,
-          [&](int co, int m, f4 v) {
-              *reinterpret_cast<f4*>(
-                  a.y + ((((int64_t)b * a.C2 + co) * a.D2 + s0) * S2 + m) * NB + i0) = v;
-          });
+    layer(y1, smem + a.lds_w2, bs_layer2(a, g), a.b2, a.act2, [&](int co, int m, f4 v) {
+        *reinterpret_cast<f4*>(a.y + bs_y_ofs(a, g, NB, co, m, i0)) = v;
+    });
 }
 
 }  // namespace

@@ -87,6 +87,7 @@ static void on_launch(const cliff::LaunchPlan& p, void*)
     switch (p.kind) {
     case cliff::LAUNCH_CONV_MFMA: check_conv_mfma(p); break;
     case cliff::LAUNCH_CONV1D_MFMA: check_conv1d(p); break;
+    case cliff::LAUNCH_BLOCK_SMALL: check_block_small(p); break;
     default: check_generic(p); break;
     }
 }

@@ -10,8 +10,8 @@ matrix-core convolution (k = 2, 3) that is every direct global->LDS load in
 bounds, every LDS word a fragment reads written by the stage with the input
 or filter element the product needs, every output stored once in bounds
 (tests/hostcheck/check_conv_mfma.cpp); the same for the 1-D matrix-core
-convolution (check_conv1d.cpp); the other kernels' launch shapes are checked
-for now.
+convolution (check_conv1d.cpp) and the fused small block
+(check_block_small.cpp); the other kernels' launch shapes are checked.
 
 Cases: the GPU parity shapes with every tile shape forced, the benchmark's
 workloads at full size, the random sweeps' draws (convolutions and blocks),
