@@ -9,6 +9,7 @@
 // written once is accessed non-temporally.
 #include <stdio.h>
 
+#include "act_geom.hpp"
 #include "common.hpp"
 #include "epilogue.hpp"
 
@@ -18,20 +19,7 @@ namespace {
 typedef float vf2 __attribute__((ext_vector_type(2)));
 typedef float vf4 __attribute__((ext_vector_type(4)));
 
-#ifndef CLIFF_ACT_VPT
-#define CLIFF_ACT_VPT 2  // measured: 2 is best or tied at 0.27-1.3 GB per call
-#endif
-constexpr int ACT_THREADS = 256;
-constexpr int ACT_VPT = CLIFF_ACT_VPT;  // multivectors per thread
 
-struct ActKArgs {
-    const float* x;
-    float* y;
-    int64_t P;       // positions per (b, c)
-    int64_t n_pblk;  // workgroups per (b, c)
-    int C;
-    ActParams act;
-};
 
 template <int NB>
 struct MV {
@@ -76,25 +64,24 @@ __device__ inline void store_mv(float* p, const MV<NB>& m)
 template <int NB>
 __global__ __launch_bounds__(ACT_THREADS) void act_kernel(ActKArgs a)
 {
-    const int64_t bc = blockIdx.x / a.n_pblk;  // (b, c) of this workgroup
-    const int64_t pblk = blockIdx.x - bc * a.n_pblk;
+    // (b, c) of this workgroup and its positions: act_geom.hpp
+    const int64_t bc = act_bc(a, blockIdx.x);
     const int c = (int)(bc % a.C);
     float coef[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) coef[i] = gate_coef(a.act, gate_slot(a.act, i), c);
 
-    const int64_t p0 = pblk * (ACT_THREADS * ACT_VPT) + threadIdx.x;
-    const float* xb = a.x + bc * a.P * NB;
-    float* yb = a.y + bc * a.P * NB;
+    const float* xb = a.x + act_base(a, bc, NB);
+    float* yb = a.y + act_base(a, bc, NB);
     MV<NB> m[ACT_VPT];
 #pragma unroll
     for (int v = 0; v < ACT_VPT; ++v) {
-        const int64_t p = p0 + v * ACT_THREADS;
+        const int64_t p = act_pos(a, blockIdx.x, bc, threadIdx.x, v);
         if (p < a.P) m[v] = load_mv<NB>(xb + p * NB);
     }
 #pragma unroll
     for (int v = 0; v < ACT_VPT; ++v) {
-        const int64_t p = p0 + v * ACT_THREADS;
+        const int64_t p = act_pos(a, blockIdx.x, bc, threadIdx.x, v);
         if (p < a.P) {
             float part = 0.f;
 #pragma unroll

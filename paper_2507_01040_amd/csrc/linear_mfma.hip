@@ -30,6 +30,7 @@
 
 #include "common.hpp"
 #include "epilogue.hpp"
+#include "linear_geom.hpp"
 
 namespace cliff {
 namespace {
@@ -37,18 +38,6 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
 
-struct LinArgs {
-    const float* x;
-    const float* w;
-    const float* bias;
-    float* y;
-    int64_t B;     // positions (rows of X and Y)
-    int64_t n_wt;  // wave tiles: ceil(B / (16 NWW))
-    int C_in;
-    int WP;        // LDS floats per input channel of the weight (N plus padding)
-    SignMasks sign;
-    ActParams act;
-};
 
 // NB blades; RT = N / 16 row tiles (all of them per wave); KQ = K / 16
 // chunks; NWW 16-position column tiles per wave tile; PF chunks of prefetch.
@@ -104,24 +93,20 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
     const int waves = blockDim.x >> 6;
     const int n = lane & 15, r = lane >> 4;
     constexpr int K = KQ * 16;
-    const int WP = a.WP;
-    const int QS = (16 / NB) * WP;  // LDS floats per K chunk (16 / NB channels)
 
-    // LDS: the raw weight [C_in][N] in rows of WP floats (NEG: then its
-    // negation, in the same layout); then the bias [N]
-    // (zero without one), each (co, blade)'s gate coefficient [N] and each
-    // channel's gate bias [N / N_B] (Linear mode; zero otherwise).  The
-    // epilogue reads them from here: a global load issued after the input
-    // prefetch would have to wait for all of it.
-    const int wfloats = a.C_in * WP;
-    float* bl = wl + (NEG ? 2 : 1) * wfloats;
+    // LDS (linear_geom.hpp): the raw weight (NEG: and its negation); then
+    // the bias (zero without one), the gate coefficients and the gate biases
+    // (Linear mode; zero otherwise).  The epilogue reads them from here: a
+    // global load issued after the input prefetch would have to wait for all
+    // of it.
+    const int wfloats = lin_wfloats(a);
+    float* bl = wl + lin_tail(a, NEG);
     float* cl = bl + N;
     float* gl = cl + N;
     for (int e = tid; e < a.C_in * (N / 4); e += blockDim.x) {
-        const int ci = e / (N / 4), c4 = e - ci * (N / 4);
         const f4 v = *reinterpret_cast<const f4*>(a.w + (int64_t)e * 4);
-        *reinterpret_cast<f4*>(wl + ci * WP + c4 * 4) = v;
-        if (NEG) *reinterpret_cast<f4*>(wl + wfloats + ci * WP + c4 * 4) = -v;
+        *reinterpret_cast<f4*>(wl + lin_w_lds(a, N, e)) = v;
+        if (NEG) *reinterpret_cast<f4*>(wl + wfloats + lin_w_lds(a, N, e)) = -v;
     }
     for (int e = tid; e < N; e += blockDim.x) {
         bl[e] = a.bias ? a.bias[e] : 0.f;
@@ -130,18 +115,16 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
     }
     __syncthreads();
 
-    // A fragment lane (row n of a row tile, K slot r): row = (co, i) with
-    // i = n % NB; step t reads input channel (4 r + t) / NB of the chunk and
-    // blade j = (4 r + t) % NB, i.e. weight blade src(i, j) with sign s(i, j).
+    // A fragment lane (row n of a row tile, K slot r): step t of a chunk
+    // reads weight blade src(i, j) with sign s(i, j) (linear_geom.hpp; NEG:
+    // from the copy of its sign)
     const int i = n % NB;
     int abase[4];
     float sg[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-        const int k0 = 4 * r + t, ci0 = k0 / NB, j = k0 % NB;
-        abase[t] = ci0 * WP + (n - i) + src_blade(NB, i, j);
-        sg[t] = sign_of(a.sign, i * NB + j);
-        if (NEG && sg[t] < 0.f) abase[t] += wfloats;  // the negated copy
+        sg[t] = sign_of(a.sign, i * NB + (4 * r + t) % NB);
+        abase[t] = lin_a_base(a, NB, n, r, t, NEG && sg[t] < 0.f);
     }
 
     const int64_t stride = (int64_t)gridDim.x * waves;
@@ -149,10 +132,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
     if (t >= a.n_wt) return;  // wave-uniform, after the only barrier
     // row of X for column tile nw of wave tile tt (past B: the last row,
     // loaded but never stored)
-    auto xrow = [&](int64_t tt, int nw) {
-        const int64_t m = tt * TP + nw * 16 + n;
-        return a.x + (m < a.B ? m : a.B - 1) * K + 4 * r;
-    };
+    auto xrow = [&](int64_t tt, int nw) { return a.x + lin_x_row(a, K, TP, tt, nw, n, r); };
     f4 ring[PF][NWW];
 #pragma unroll
     for (int p = 0; p < PF; ++p)
@@ -162,7 +142,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
     // A values of the next step, read one step ahead
     float fa[2][RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) fa[0][rt] = wl[abase[0] + 16 * rt];
+    for (int rt = 0; rt < RT; ++rt) fa[0][rt] = wl[abase[0] + lin_a_step(a, NB, 0, rt)];
     // N = K = 64: every step's signed A values stay in registers (64 per
     // lane), read and signed once, so the tile loop has no LDS reads and no
     // multiplies
@@ -173,7 +153,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
         for (int s = 0; s < 4 * KQ; ++s)
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                const float w = wl[abase[s % 4] + (s / 4) * QS + 16 * rt];
+                const float w = wl[abase[s % 4] + lin_a_step(a, NB, s, rt)];
                 areg[s][rt] = NEG ? w : w * sg[s % 4];
             }
     }
@@ -212,7 +192,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
                 const int s1 = (s + 1) % (4 * KQ);
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt)
-                    fa[cur ^ 1][rt] = wl[abase[s1 % 4] + (s1 / 4) * QS + 16 * rt];
+                    fa[cur ^ 1][rt] = wl[abase[s1 % 4] + lin_a_step(a, NB, s1, rt)];
             }
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
@@ -267,7 +247,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
         // around a store would make the compiler assume the store might not
         // have been issued and wait for the next tile's prefetch too early).
         const int64_t m0 = t * TP;
-        const int64_t rows = a.B - m0 < TP ? a.B - m0 : TP;
+        const int64_t rows = lin_y_rows(a, TP, t);
         // (raw descriptor: stride 0, size in bytes; word 3 = 32-bit data
         // format, the value CDNA's buffer instructions expect for raw access)
         const __amdgpu_buffer_rsrc_t ydesc = __builtin_amdgcn_make_buffer_rsrc(
@@ -305,7 +285,7 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
                     }
                 }
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), ydesc,
-                                                       ((nw * 16 + n) * N + row0) * 4, 0,
+                                                       lin_y_byte(N, nw, n, row0), 0,
                                                        CLIFF_LIN_STORE_AUX);
             }
         }
@@ -321,6 +301,10 @@ __global__ __launch_bounds__(NT, WAVES) void linear_mfma_kernel(LinArgs a)
 template <int NB, int RT, int KQ, int NWW, int PF, int WAVES, bool NEG, int NT = 256>
 int linear_occupancy(int64_t lds)
 {
+    // With a launch observer (the host-side checker, no GPU): the residency
+    // the launch bounds ask for (WAVES waves per SIMD), within the LDS.
+    if (launch_observer)
+        return lds > 160 * 1024 ? 0 : (int)std::min<int64_t>(4 * WAVES * 64 / NT, 160 * 1024 / lds);
     static std::atomic<int64_t> cache{0};
     auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, NEG, NT>;
     const int64_t c = cache.load(std::memory_order_relaxed);

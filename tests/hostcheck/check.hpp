@@ -43,6 +43,8 @@ const Buffer* find_buffer(const void* p);
 void check_conv_mfma(const cliff::LaunchPlan& p);
 void check_conv1d(const cliff::LaunchPlan& p);
 void check_block_small(const cliff::LaunchPlan& p);
+void check_act(const cliff::LaunchPlan& p);
+void check_linear(const cliff::LaunchPlan& p);
 void check_generic(const cliff::LaunchPlan& p);
 
 }  // namespace hostcheck

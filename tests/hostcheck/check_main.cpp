@@ -88,6 +88,8 @@ static void on_launch(const cliff::LaunchPlan& p, void*)
     case cliff::LAUNCH_CONV_MFMA: check_conv_mfma(p); break;
     case cliff::LAUNCH_CONV1D_MFMA: check_conv1d(p); break;
     case cliff::LAUNCH_BLOCK_SMALL: check_block_small(p); break;
+    case cliff::LAUNCH_ACT: check_act(p); break;
+    case cliff::LAUNCH_LINEAR_MFMA: check_linear(p); break;
     default: check_generic(p); break;
     }
 }

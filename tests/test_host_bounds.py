@@ -10,8 +10,10 @@ matrix-core convolution (k = 2, 3) that is every direct global->LDS load in
 bounds, every LDS word a fragment reads written by the stage with the input
 or filter element the product needs, every output stored once in bounds
 (tests/hostcheck/check_conv_mfma.cpp); the same for the 1-D matrix-core
-convolution (check_conv1d.cpp) and the fused small block
-(check_block_small.cpp); the other kernels' launch shapes are checked.
+convolution (check_conv1d.cpp), the fused small block
+(check_block_small.cpp), the streamed linear layer (check_linear.cpp) and the
+standalone activation (check_act.cpp); the direct kernel's launch shapes are
+checked.
 
 Cases: the GPU parity shapes with every tile shape forced, the benchmark's
 workloads at full size, the random sweeps' draws (convolutions and blocks),
@@ -187,3 +189,62 @@ def test_conv1d_176_position_tile():
         f = res.split()
         assert f[4] == "2", (label, res)  # one 1-D matrix-core launch
         assert int(f[5].split(".")[4]) == nw, (label, res)
+
+
+def act_line(nb, B, C, Pn, act):
+    return "act %d %d %d %d %s" % (nb, B, C, Pn, act_field(act))
+
+
+def test_standalone_activation():
+    # the GPU parity shapes (every N_B and mode, P = 1), positions around the
+    # 512 per workgroup, the benchmark's activation shapes and the > 2^31
+    # element in-place case (the checker walks every workgroup of grids up to
+    # 2^15 and counts each output multivector; larger grids are sampled)
+    cases = []
+    for nb in (2, 4, 8):
+        for mode in (P.AGG_LINEAR, P.AGG_SUM, P.AGG_MEAN):
+            K = max(1, nb - 1)
+            for (B, C, Pn) in ((3, 7, 11), (5, 9, 1), (2, 3, 513), (1, 2, 1024)):
+                cases.append(("nb %d mode %d B %d C %d P %d" % (nb, mode, B, C, Pn),
+                              act_line(nb, B, C, Pn, (mode, tuple(range(K))))))
+    cases.append(("bench linear", act_line(4, 8, 64, 16384, (P.AGG_LINEAR, (0, 1, 2, 3)))))
+    cases.append(("bench mean", act_line(8, 8, 64, 39304, (P.AGG_MEAN, tuple(range(8))))))
+    cases.append(("> 2^31 elements", act_line(4, 520, 64, 126 * 126,
+                                              (P.AGG_LINEAR, (0, 1, 2, 3)))))
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        assert res.split()[4] == "6", (label, res)  # one activation launch
+
+
+def test_streamed_linear_layers():
+    # the streamed linear kernel (d_image = d_filter = 1, forced or chosen):
+    # the GPU tests' widths, rectangular layers and batch sizes (one tile and
+    # a ragged last tile), many tiles per wave, the random draws and the
+    # benchmark's layers (sampled tiles past 2^15; every wave's A reads)
+    import test_linear_stream_gpu as LS
+    import test_random_linear_gpu as RL
+    cases = []
+    S = P.ALGO_MFMA_STREAM
+
+    def add(label, g, B, C_in, C_out, algo, act=None):
+        cases.append((label, conv_line(len(g), g, B, C_in, C_out, 1, 1, algo, act)))
+    for g, C in LS.WIDTHS:
+        nb = 1 << len(g)
+        for B in (1, 17, 1000):
+            add("width %s C %d B %d" % (g, C, B), g, B, C, C, S)
+        add("width %s C %d many tiles" % (g, C), g, (1 << 20) // (C * nb // 32) + 13, C, C, S)
+        add("width %s C %d linear gate" % (g, C), g, 5000, C, C, S,
+            (P.AGG_LINEAR, tuple(range(nb))))
+    for g, C_in, C_out in LS.RECT:
+        for B in (37, 1000):
+            add("rect %s %d->%d B %d" % (g, C_in, C_out, B), g, B, C_in, C_out, S)
+    for (g, C_in, C_out, B, has_bias, act, seed) in RL.draw_layers():
+        add("random %s %d->%d B %d" % (g, C_in, C_out, B), g, B, C_in, C_out, P.ALGO_AUTO,
+            None if act is None else act)
+    for k, B in ((2, 1 << 20), (3, 1 << 19), (1, 1 << 21)):
+        g = (1,) * k
+        add("benchmark k %d" % k, g, B, 32, 32, P.ALGO_AUTO)
+    out = _run_cases(cases, lambda line: False)
+    for (label, line), res in zip(cases, out):
+        if int(line.split()[2 + int(line.split()[1]) + 5]) == S:
+            assert res.split()[4] == "4", (label, res)  # one streamed-linear launch
