@@ -7,45 +7,20 @@
 #include <stdio.h>
 
 #include "common.hpp"
+#include "direct_geom.hpp"
 #include "epilogue.hpp"
 
 namespace cliff {
 namespace {
-
-struct DirectArgs {
-    const float* x;
-    const float* w;
-    const float* bias;
-    float* y;
-    int64_t total;  // B * C_out * d_out^k
-    int C_in, C_out, D, Do, df;
-    int64_t npos, nimg, ntap;  // d_out^k, d_image^k, d_filter^k
-    SignMasks sign;
-    ActParams act;
-};
 
 template <int KD, int NB>
 __global__ __launch_bounds__(256) void conv_direct_kernel(DirectArgs a)
 {
     const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (t >= a.total) return;
-    const int64_t sp = t % a.npos;
-    const int64_t bc = t / a.npos;
-    const int co = (int)(bc % a.C_out);
-    const int64_t b = bc / a.C_out;
-
-    int pc[KD];
-    {
-        int64_t r = sp;
-#pragma unroll
-        for (int d = KD - 1; d >= 0; --d) {
-            pc[d] = (int)(r % a.Do);
-            r /= a.Do;
-        }
-    }
-    int64_t pbase = 0;  // flat input index of position p (tap q = 0)
-#pragma unroll
-    for (int d = 0; d < KD; ++d) pbase = pbase * a.D + pc[d];
+    // (batch entry, output channel, position) and offsets: direct_geom.hpp
+    const DirectThread d = direct_thread<KD>(a, t);
+    const int co = d.co;
 
     float sg[NB][NB];
 #pragma unroll
@@ -58,16 +33,10 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(DirectArgs a)
     for (int i = 0; i < NB; ++i) o[i] = 0.f;
 
     for (int ci = 0; ci < a.C_in; ++ci) {
-        const float* xb = a.x + ((b * a.C_in + ci) * a.nimg + pbase) * NB;
-        const float* wb = a.w + ((int64_t)ci * a.C_out + co) * a.ntap * NB;
+        const float* xb = a.x + direct_x(a, d, ci, NB);
+        const float* wb = a.w + direct_w(a, d, ci, NB);
         for (int64_t q = 0; q < a.ntap; ++q) {
-            int64_t qoff = 0, r = q, scale = 1;
-#pragma unroll
-            for (int d = KD - 1; d >= 0; --d) {
-                qoff += (r % a.df) * scale;
-                r /= a.df;
-                scale *= a.D;
-            }
+            const int64_t qoff = direct_qoff<KD>(a, q);
             float wv[NB], xv[NB];
 #pragma unroll
             for (int i = 0; i < NB; ++i) {

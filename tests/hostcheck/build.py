@@ -21,7 +21,8 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 LIB_SOURCES = ["api.cpp", "conv_mfma.hip", "conv1d_mfma.hip", "conv_direct.hip", "act.hip",
                "block_small.hip", "block_noalloc.hip", "linear_mfma.hip", "mfma_probe.hip"]
 CHECK_SOURCES = ["check_main.cpp", "check_conv_mfma.cpp", "check_conv1d.cpp", "check_block_small.cpp",
-                 "check_act.cpp", "check_linear.cpp", "check_generic.cpp"]
+                 "check_act.cpp", "check_linear.cpp", "check_direct.cpp",
+                 "check_generic.cpp"]
 # sanitizers on the host side only; each -fsanitize= behind -Xarch_host
 FLAGS = ["--offload-arch=gfx950", "-O2", "-g", "-std=c++17", "-fPIC", "-fno-omit-frame-pointer",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

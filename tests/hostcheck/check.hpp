@@ -45,6 +45,7 @@ void check_conv1d(const cliff::LaunchPlan& p);
 void check_block_small(const cliff::LaunchPlan& p);
 void check_act(const cliff::LaunchPlan& p);
 void check_linear(const cliff::LaunchPlan& p);
+void check_direct(const cliff::LaunchPlan& p);
 void check_generic(const cliff::LaunchPlan& p);
 
 }  // namespace hostcheck

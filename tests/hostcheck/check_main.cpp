@@ -90,6 +90,7 @@ static void on_launch(const cliff::LaunchPlan& p, void*)
     case cliff::LAUNCH_BLOCK_SMALL: check_block_small(p); break;
     case cliff::LAUNCH_ACT: check_act(p); break;
     case cliff::LAUNCH_LINEAR_MFMA: check_linear(p); break;
+    case cliff::LAUNCH_CONV_DIRECT: check_direct(p); break;
     default: check_generic(p); break;
     }
 }

@@ -12,8 +12,8 @@ or filter element the product needs, every output stored once in bounds
 (tests/hostcheck/check_conv_mfma.cpp); the same for the 1-D matrix-core
 convolution (check_conv1d.cpp), the fused small block
 (check_block_small.cpp), the streamed linear layer (check_linear.cpp) and the
-standalone activation (check_act.cpp); the direct kernel's launch shapes are
-checked.
+standalone activation (check_act.cpp) and the direct (vector-ALU) kernel
+(check_direct.cpp).
 
 Cases: the GPU parity shapes with every tile shape forced, the benchmark's
 workloads at full size, the random sweeps' draws (convolutions and blocks),
