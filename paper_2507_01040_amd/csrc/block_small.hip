@@ -113,7 +113,7 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             const bool cvalid = co < Cout;
             const int co_c = min(co, Cout - 1);
             const bool lin = act.mode == CLIFF_AGG_LINEAR;
-            const f4 bv = *reinterpret_cast<const f4*>(bias ? bias + co_c * NB + i0 : a.x);
+            const f4 bias_v = *reinterpret_cast<const f4*>(bias ? bias + co_c * NB + i0 : a.x);
             float gw[4];
 #pragma unroll
             for (int r2 = 0; r2 < 4; ++r2)
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(BS_THREADS) void block_small_kernel(BlockArgs a)
             // gate_coef's weights: the Linear gate's, 1 for Sum and Mean, 0
             // outside the subset)
             const int m = tl.m;
-            if (cvalid && bias) v += bv;
+            if (cvalid && bias) v += bias_v;
             if (has_act) {
                 float part = 0.f;
                 if (cvalid) {
