@@ -304,7 +304,9 @@ int linear_occupancy(int64_t lds)
     // With a launch observer (the host-side checker, no GPU): the residency
     // the launch bounds ask for (WAVES waves per SIMD), within the LDS.
     if (launch_observer)
-        return lds > 160 * 1024 ? 0 : (int)std::min<int64_t>(4 * WAVES * 64 / NT, 160 * 1024 / lds);
+        return lds < 1 || lds > 160 * 1024
+                   ? 0
+                   : (int)std::min<int64_t>(4 * WAVES * 64 / NT, 160 * 1024 / lds);
     static std::atomic<int64_t> cache{0};
     auto kern = linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, NEG, NT>;
     const int64_t c = cache.load(std::memory_order_relaxed);
