@@ -248,6 +248,14 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
                              for l, t in zip(timed, per_layer)]}
     res["frac_of_fp32_mfma_peak"] = round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4)
     res["graph_ms_per_step"] = round(r.time_graph(max(steps, 20), warmup), 4)
+    g_act = None
+    if sum(per_layer) < 0.1:
+        # a few-microsecond kernel: events around single launches and
+        # single-step graphs measure mostly the host and launch path, so it
+        # also runs as graphs of 32 back-to-back steps (GPU time per step)
+        g_act = r.time_graph(256, warmup, per_graph=32)
+        res["graph32_ms_per_step"] = round(g_act, 4)
+        res["graph32_useful_gflops"] = round(flops / (g_act * 1e-3) / 1e9, 1)
     if w.entry == "block2":
         # the same block as two clifford_conv_nd launches through the workspace
         import paper_2507_01040_amd as P
@@ -261,13 +269,9 @@ def measure(name: str, steps: int, warmup: int, epilogue_overhead: bool = False)
         plain = Runner(w, fuse_act=False)
         ms_plain, per_plain = plain.time(steps, warmup)
         res["bias_only_kernel_ms"] = [round(v, 4) for v in per_plain]
-        if sum(per_layer) < 0.1:
-            # a few-microsecond kernel: events around single launches measure
-            # mostly the host launch path, so both variants run as graphs of
-            # 32 back-to-back steps (GPU time per step, no host gaps)
-            g_act = r.time_graph(256, warmup, per_graph=32)
+        if g_act is not None:
+            # both variants as graphs of 32 back-to-back steps
             g_plain = plain.time_graph(256, warmup, per_graph=32)
-            res["graph32_ms_per_step"] = round(g_act, 4)
             res["bias_only_graph32_ms_per_step"] = round(g_plain, 4)
             res["fused_act_overhead"] = round(g_act / g_plain - 1.0, 4)
             res["fused_act_overhead_from"] = "graphs of 32 steps"
