@@ -397,12 +397,26 @@ def measure_linear(k: int, B: int, C: int, steps: int = 30, warmup: int = 10):
         e1.record()
     torch.cuda.synchronize()
     ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
+    # a plain device copy of the input into a buffer of the output's size (the
+    # layer's streamed bytes; C_in = C_out): the HBM rate reachable in practice
+    # at this size, which is past the on-package cache
+    warm(lambda: out.copy_(x), warmup, torch)
+    for e0, e1 in ev:
+        e0.record()
+        out.copy_(x)
+        e1.record()
+    torch.cuda.synchronize()
+    ms_copy = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
     flops = 2 * B * C * C * nb * nb
     nbytes = 4 * (x.numel() + w.numel() + b.numel() + out.numel())
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    copy_gbs = 8 * x.numel() / (ms_copy * 1e-3) / 1e9
     return {"k": k, "B": B, "C_in": C, "C_out": C, "kernel_ms": round(ms, 4),
             "useful_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
             "frac_of_fp32_mfma_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA_TFLOPS, 4),
-            "GB_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+            "GB_s": round(gbs, 1), "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "device_copy_GB_s": round(copy_gbs, 1),
+            "frac_of_device_copy": round(gbs / copy_gbs, 4)}
 
 
 def main():
