@@ -593,13 +593,21 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 // the 64-channel tile with 10 staging slots, for stages that need them
 // (large images or filters; 6 slots measured 0.4 % faster where they suffice)
 #define CLIFF_W2_S10 4, 1, 4, 8, 10, 2, 1, 80
-// the 64-channel tile 96 positions wide (4x6 tiles per wave)
+// the 64-channel tile 96 and 112 positions wide (4x6, 4x7 tiles per wave)
 #define CLIFF_W2_96 4, 1, 4, 6, 6, 2, 1, 80
+#define CLIFF_W2_112 4, 1, 4, 7, 6, 2, 1, 80
+#ifndef CLIFF_W2_112ON
+#define CLIFF_W2_112ON 1
+#endif
 // the d_filter = 1 (linear) wide kernels keep 6 slots: with 9 they spill
 #define CLIFF_W2_LIN 4, 1, 4, 8, 6, 2, 1, 80
 #define CLIFF_W2_32_LIN 2, 2, 4, 8, 6, 2, 1, 80
 #define CLIFF_W3_32 4, 1, 4, 8, 6, 2  // k = 3, 3x3x3 wide variant for 16 < C_out <= 32
 #define CLIFF_W3_32_96 4, 1, 4, 6, 6, 2  // the same with 96 positions (6 tiles per wave)
+#define CLIFF_W3_32_112 4, 1, 4, 7, 6, 2  // ... and 112 (7 tiles per wave)
+#ifndef CLIFF_W3_112
+#define CLIFF_W3_112 1
+#endif
 #define CLIFF_MEDIUM2 4, 1, 4, 2, 8, 4
 #define CLIFF_MEDIUM3 4, 1, 4, 2, 8, 3
 #define CLIFF_NARROW 1, 4, 2, 4, 8, 2
@@ -662,6 +670,7 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
         // row-aligned blocks counted where they are snug, as the kernel takes
         // them; the 96 tile, with 24 MFMA tiles per wave, never takes them)
         using W128 = Shape<NB, CLIFF_W2>;
+        using W112 = Shape<NB, CLIFF_W2_112>;
         using W96 = Shape<NB, CLIFF_W2_96>;
         const int64_t Do = p.d_out, M = p.B * Do * Do;
         const double useful = 2.0 * M * p.C_out * NB * p.C_in * NB * (double)(p.d_filter * p.d_filter);
@@ -673,10 +682,17 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
         auto fill = [&](int64_t n) {
             return (double)n / (double)(((n + cus - 1) / cus) * cus);
         };
-        if (CLIFF_W2_WIDTH_MODEL && p.mfma_shape < 0 && useful >= 1e9 && cus > 0 &&
-            fill(nblk(W96::pos, false)) > fill(nblk(W128::pos, true)))
-            return run_shapes<KD, NB, DF, W96, Shape<NB, CLIFF_W2_S10>, Shape<NB, CLIFF_W2_32>>(
-                p, stream);
+        if (CLIFF_W2_WIDTH_MODEL && p.mfma_shape < 0 && useful >= 1e9 && cus > 0) {
+            const double f128 = fill(nblk(W128::pos, true));
+            const double f112 = CLIFF_W2_112ON ? fill(nblk(W112::pos, false)) : 0.0;
+            const double f96 = fill(nblk(W96::pos, false));
+            if (f112 > f128 && f112 >= f96)
+                return run_shapes<KD, NB, DF, W112, Shape<NB, CLIFF_W2_S10>,
+                                  Shape<NB, CLIFF_W2_32>>(p, stream);
+            if (f96 > f128)
+                return run_shapes<KD, NB, DF, W96, Shape<NB, CLIFF_W2_S10>,
+                                  Shape<NB, CLIFF_W2_32>>(p, stream);
+        }
         return run_shapes<KD, NB, DF, W128, Shape<NB, CLIFF_W2_S10>,
                           Shape<NB, CLIFF_W2_32>>(p, stream);
     } else {
@@ -692,6 +708,7 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
                 // -> 32 (2048 blocks of 128) -4 % with 96; d 24 -> 22, where
                 // only 96 makes the wide tile worth taking, +13 %.
                 using W128 = Shape<NB, CLIFF_W3_32>;
+                using W112 = Shape<NB, CLIFF_W3_32_112>;
                 using W96 = Shape<NB, CLIFF_W3_32_96>;
                 int64_t M = p.B;
                 for (int t = 0; t < KD; ++t) M *= p.d_out;
@@ -700,9 +717,13 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
                 auto fill = [&](int64_t n) {
                     return (double)n / (double)(((n + cus - 1) / cus) * cus);
                 };
-                if (p.mfma_shape < 0 && useful >= 1e9 && cus > 0 &&
-                    fill(W96::blocks(p, M)) > fill(W128::blocks(p, M)))
-                    return run_shapes<KD, NB, DF, W96>(p, stream);
+                if (p.mfma_shape < 0 && useful >= 1e9 && cus > 0) {
+                    const double f128 = fill(W128::blocks(p, M));
+                    const double f112 = CLIFF_W3_112 ? fill(W112::blocks(p, M)) : 0.0;
+                    const double f96 = fill(W96::blocks(p, M));
+                    if (f112 > f128 && f112 >= f96) return run_shapes<KD, NB, DF, W112>(p, stream);
+                    if (f96 > f128) return run_shapes<KD, NB, DF, W96>(p, stream);
+                }
                 return run_shapes<KD, NB, DF, W128>(p, stream);
             }
         return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W3>>(p, stream);

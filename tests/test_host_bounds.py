@@ -191,6 +191,29 @@ def test_conv1d_176_position_tile():
         assert int(f[5].split(".")[4]) == nw, (label, res)
 
 
+def test_wide_112_position_tiles():
+    # The 112-position forms of the 2D 64-channel and 3D 32-channel wide tiles
+    # (template NW = 7): the quantisation model takes them where their blocks
+    # fill the last round of CUs best, keeps 128 (the headline's row-aligned
+    # blocks, the 2D block's first layer, 3D d 34) or 96 (3D d 32, 2D d 96)
+    # elsewhere, and the checker walks each choice.
+    cases, want = [], []
+    for k, g, B, C_in, C_out, d, nw in ((2, (1, 1), 8, 4, 64, 84, 7), (2, (1, 1), 16, 64, 64, 44, 7),
+                                        (2, (1, 1), 4, 64, 64, 148, 7), (2, (-1, 0), 8, 4, 64, 102, 7),
+                                        (2, (1, 1), 8, 64, 64, 128, 8), (2, (1, -1), 8, 64, 64, 130, 8),
+                                        (2, (1, 1), 8, 4, 64, 96, 6), (3, (1, 1, 1), 8, 4, 32, 24, 7),
+                                        (3, (1, -1, 1), 8, 32, 32, 36, 7), (3, (1, 1, 1), 8, 32, 32, 42, 7),
+                                        (3, (1, 1, 1), 8, 32, 32, 32, 6), (3, (1, 1, 1), 8, 32, 32, 34, 8)):
+        cases.append(("%dD B %d C %d->%d d %d" % (k, B, C_in, C_out, d),
+                      conv_line(k, g, B, C_in, C_out, d, 3, P.ALGO_AUTO)))
+        want.append(nw)
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res, nw in zip(cases, out, want):
+        f = res.split()
+        assert f[4] == "1", (label, res)  # one matrix-core convolution launch
+        assert int(f[5].split(".")[7]) == nw, (label, res)
+
+
 def act_line(nb, B, C, Pn, act):
     return "act %d %d %d %d %s" % (nb, B, C, Pn, act_field(act))
 

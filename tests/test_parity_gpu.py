@@ -432,6 +432,23 @@ def test_3d_wide_96_positions(g):
         assert_parity(got, ref, what="algo %d" % algo)
 
 
+# The 112-position forms of the wide tiles (7 MFMA tiles per wave), which the
+# automatic choice takes where their blocks fill the last round of CUs best:
+# 2D, 64 output channels, B = 8, d 84 -> 82 (481 blocks of 112 positions,
+# 94 % of 2 rounds on 256 CUs, against 421 of 128 at 82 % and 561 of 96 at
+# 73 % of 3); 3D, 32 output channels, B = 8, d 24 -> 22 (761 blocks, 99 % of
+# 3 rounds, against 666 of 128 and 888 of 96 at 87 %).  Compared in full with
+# the oracle.
+@pytest.mark.parametrize("case", [((1, 1), 64, 84), ((-1, 0), 64, 84),
+                                  ((1, 1, 1), 32, 24), ((1, -1, 0), 32, 24)], ids=str)
+def test_wide_112_positions(case):
+    g, C_out, D = case
+    B, C_in, df = 8, 4, 3
+    s, x, f, b = _case(210, g, (B, C_in, C_out, D, df))
+    y = gpu_conv(g, x, f, b, algo=P.ALGO_AUTO)
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(case))
+
+
 # 2D, >= 1 GFLOP, 64 output channels: the automatic choice takes the wide
 # tile at 96 positions per block where its blocks fill the last round of CUs
 # better than 128 (here 737 blocks, 96 % of 3 rounds on 256 CUs, against
