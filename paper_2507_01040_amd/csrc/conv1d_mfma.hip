@@ -85,11 +85,19 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
     const int span2 = a.span2;
     const int wch = g.wch;  // floats per channel of filters
     // 32-bit byte offsets of each slot's source from the stage's bases
+    // (slots past a full stage's floats, a uniform test, load nothing)
+    const int x_floats = a.cc * span2, w_floats = a.cc * wch;
     uint32_t xoffb[SIN], woffb[SW];
 #pragma unroll
-    for (int t = 0; t < SIN; ++t) xoffb[t] = c1_xoffb(TL, a, g, (t * NT + tid) * FX);
+    for (int t = 0; t < SIN; ++t) {
+        xoffb[t] = 0;
+        if (t * NT * FX < x_floats) xoffb[t] = c1_xoffb(TL, a, g, (t * NT + tid) * FX);
+    }
 #pragma unroll
-    for (int t = 0; t < SW; ++t) woffb[t] = c1_woffb(TL, a, g, (t * NT + tid) * FW);
+    for (int t = 0; t < SW; ++t) {
+        woffb[t] = 0;
+        if (t * NT * FW < w_floats) woffb[t] = c1_woffb(TL, a, g, (t * NT + tid) * FW);
+    }
     const char* xbase = reinterpret_cast<const char*>(a.x + c1_x_base(a, g));
     const char* wbase = reinterpret_cast<const char*>(a.w + c1_w_base(g));
     const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -100,7 +108,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
         const char* ws = wbase + c1_stage_w(a, g, s) * 4;
 #pragma unroll
         for (int t = 0; t < SIN; ++t) {
-            if (c1_x_loads(a, (t * NT + tid) * FX, nv)) {
+            if (t * NT * FX < x_floats && c1_x_loads(a, (t * NT + tid) * FX, nv)) {
                 auto* dst = (__attribute__((address_space(3))) void*)(
                     smem + c1_lds_x(TL, a, buf, t, wave_u));
                 const float* src = reinterpret_cast<const float*>(xs + xoffb[t]);
@@ -112,7 +120,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES) void conv1d_mfma_kerne
         }
 #pragma unroll
         for (int t = 0; t < SW; ++t) {
-            if (c1_w_loads(TL, g, (t * NT + tid) * FW, woffb[t], nv)) {
+            if (t * NT * FW < w_floats && c1_w_loads(TL, g, (t * NT + tid) * FW, woffb[t], nv)) {
                 auto* dst = (__attribute__((address_space(3))) void*)(
                     smem + c1_lds_w(TL, a, g, buf, t, wave_u));
                 // a float source pointer and literal sizes: with a char

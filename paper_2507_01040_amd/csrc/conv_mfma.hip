@@ -110,7 +110,11 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
     const int m0 = g.m0, m_end = g.m_end;
     int goff[SLOTS];
 #pragma unroll
-    for (int t = 0; t < SLOTS; ++t) goff[t] = mfma_slot_goff(TL, a, g, t * NT + tid);
+    for (int t = 0; t < SLOTS; ++t) {
+        // slots past the block's staged float4 (a uniform test) load nothing
+        goff[t] = 0;
+        if (t * NT < g.total_f4) goff[t] = mfma_slot_goff(TL, a, g, t * NT + tid);
+    }
 
     const float* xbase = a.x + mfma_x_base(TL, a, g);
     const float* wbase = a.w + mfma_w_base(TL, g);
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(64 * WCO * WPOS * WK, WAVES_PER_SIMD) void conv_mfm
         float* lbase = smem + mfma_lds_wave(a, buf, wave_u);
 #pragma unroll
         for (int t = 0; t < SLOTS; ++t) {
-            if (mfma_slot_loads(TL, g, t * NT + tid, goff[t], nv)) {
+            if (t * NT < g.total_f4 && mfma_slot_loads(TL, g, t * NT + tid, goff[t], nv)) {
                 const float* src = goff[t] >= 0 ? xs + goff[t] : ws + (-1 - goff[t]);
                 __builtin_amdgcn_global_load_lds(
                     src, (__attribute__((address_space(3))) void*)(lbase + mfma_lds_slot(TL, t)),
