@@ -153,13 +153,13 @@ ActParams to_params(const cliff_act_desc* act)
     ActParams a;
     a.mode = -1;
     a.K = 0;
-    for (int t = 0; t < 8; ++t) a.idx[t] = -1;
+    for (int b = 0; b < 8; ++b) a.slot[b] = -1;
     a.weight = nullptr;
     a.bias = nullptr;
     if (act) {
         a.mode = act->mode;
         a.K = act->K;
-        for (int t = 0; t < act->K; ++t) a.idx[t] = act->blade_idx[t];
+        for (int t = 0; t < act->K; ++t) a.slot[act->blade_idx[t]] = t;
         if (act->mode == CLIFF_AGG_LINEAR) {
             a.weight = act->weight;
             a.bias = act->bias;

@@ -40,9 +40,9 @@ __host__ __device__ inline float sign_of(const SignMasks& s, int e)
 }
 
 struct ActParams {
-    int mode;  // -1: no activation
+    int mode;     // -1: no activation
     int K;
-    int idx[8];
+    int slot[8];  // blade b's place in the gate's blade list, -1 if not in it
     const float* weight;
     const float* bias;
 };

@@ -6,13 +6,14 @@
 
 namespace cliff {
 
-// Position of blade `blade` in the gate's blade list, or -1.
+// Position of blade `blade` in the gate's blade list, or -1 (a lookup in
+// the table the host fills; for a blade known at compile time one argument
+// word, else a chain of selects).
 __device__ inline int gate_slot(const ActParams& act, int blade)
 {
-    int slot = -1;
+    int slot = act.slot[0];
 #pragma unroll
-    for (int t = 0; t < 8; ++t)
-        if (t < act.K && act.idx[t] == blade) slot = t;
+    for (int b = 1; b < 8; ++b) slot = blade == b ? act.slot[b] : slot;
     return slot;
 }
 
