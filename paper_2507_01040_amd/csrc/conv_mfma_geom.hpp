@@ -56,6 +56,33 @@ struct MfmaTile {
 // [m0, m_end) (or, with row-aligned blocks, at most P positions of one output
 // row starting at column x0) by CO_WG output channels from co0, and the slab
 // of input rows it stages per channel.
+// Quotient of non-negative ints, as an unsigned division (a shorter
+// instruction sequence than the signed one); every index divided here is
+// non-negative.
+__host__ __device__ inline int udiv(int a, int b) { return (int)((unsigned)a / (unsigned)b); }
+
+// Division of non-negative ints below 2^31 by a divisor fixed for the block,
+// through its reciprocal m = ceil(2^32 / d), formed once: the high word of
+// n m exceeds n / d by less than n / 2^32 < 1/2, so it is the quotient or one
+// more, and the sign of the remainder decides (d = 1, whose m needs 33 bits,
+// is taken apart).  Per division a multiply-high, a multiply and a compare
+// instead of a full division sequence.
+struct FastDiv {
+    int d;
+    unsigned m;
+};
+__host__ __device__ inline FastDiv fast_div(int d)
+{
+    return FastDiv{d, d > 1 ? 0xFFFFFFFFu / (unsigned)d + 1u : 0u};
+}
+__host__ __device__ inline int fdiv(int n, const FastDiv& f)
+{
+    if (f.d == 1) return n;
+    const unsigned q = (unsigned)(((unsigned long long)(unsigned)n * f.m) >> 32);
+    // q d <= n + d < 2^32: the product does not wrap in 32 unsigned bits
+    return (int)(q * (unsigned)f.d > (unsigned)n ? q - 1 : q);
+}
+
 struct MfmaBlock {
     int co0, m0, m_end, x0;
     int pl0, ylo0, len0, n_rows;  // slab: first plane, its first row, rows in it, total rows
@@ -64,6 +91,7 @@ struct MfmaBlock {
     int row_floats, lrow_floats;  // global and LDS row strides
     int cc, slab_f4, wq_f4, wch_f4, total_f4, w_lds, w_neg;
     int plane_floats, x_cstride, w_cstride;
+    FastDiv fslab, flrow, fD, fDo;  // the per-lane divisors, as reciprocals
     bool rb;
 };
 
@@ -83,16 +111,16 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     // Workgroups are dispatched round-robin over the 8 XCDs; renumbered so
     // each XCD (own L2) works through a contiguous run of position blocks,
     // whose input slabs overlap.
-    const int per = a.n_blk / 8, rem = a.n_blk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
+    const int per = a.n_blk >> 3, rem = a.n_blk & 7;
+    const int xcd = bid & 7, slot = bid >> 3;
     const int tile = xcd < rem ? xcd * (per + 1) + slot
                                : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int co_blk = tile % a.n_co_blk;
-    const int pos_blk = tile / a.n_co_blk;
+    const int pos_blk = udiv(tile, a.n_co_blk);
+    const int co_blk = tile - pos_blk * a.n_co_blk;
     g.co0 = co_blk * T.co_wg();
     g.x0 = 0;
     if (g.rb) {
-        const int seg = pos_blk % a.nseg, ry = pos_blk / a.nseg;  // output row over (b, y)
+        const int ry = udiv(pos_blk, a.nseg), seg = pos_blk - ry * a.nseg;  // output row over (b, y)
         g.x0 = seg * P;
         g.m0 = ry * Do + g.x0;
         g.m_end = g.m0 + (P < Do - g.x0 ? P : Do - g.x0);
@@ -104,9 +132,9 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     // Output rows r0..r1 (rows of d_out positions), planes pl0..pl1 (2D:
     // batch entry; 3D: (batch, z)).  Each plane contributes its output rows
     // plus d_filter - 1 halo rows; full middle planes all d_image rows.
-    const int r0 = g.m0 / Do, r1 = (g.m_end - 1) / Do;
-    g.pl0 = r0 / Do;
-    const int pl1 = r1 / Do;
+    const int r0 = udiv(g.m0, Do), r1 = udiv(g.m_end - 1, Do);
+    g.pl0 = udiv(r0, Do);
+    const int pl1 = udiv(r1, Do);
     g.ylo0 = r0 - g.pl0 * Do;
     g.len0 = g.pl0 == pl1 ? (r1 - r0) + g.df : D - g.ylo0;
     g.n_rows = g.pl0 == pl1 ? g.len0
@@ -120,11 +148,15 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
     g.total_f4 = g.cc * (g.slab_f4 + g.wch_f4);
     g.w_lds = g.cc * g.slab_f4 * 4;              // float offset of the filters in a buffer
     g.w_neg = g.w_lds + g.cc * g.wch_f4 * 4;     // NEG: of their negated copy
-    g.b0 = T.KD == 2 ? g.pl0 : g.pl0 / Do;
+    g.b0 = T.KD == 2 ? g.pl0 : udiv(g.pl0, Do);
     g.z0 = T.KD == 2 ? 0 : g.pl0 - g.b0 * Do;
     g.plane_floats = D * g.row_floats;           // one d_image x d_image plane
     g.x_cstride = g.plane_floats * (T.KD == 3 ? D : 1);  // < 2^31 (host check)
     g.w_cstride = a.C_out * g.taps_full * NB;
+    g.fslab = fast_div(g.slab_f4);
+    g.flrow = fast_div(g.lrow_floats / 4);
+    g.fD = fast_div(D);
+    g.fDo = fast_div(Do);
     return g;
 }
 
@@ -134,9 +166,9 @@ __host__ __device__ inline MfmaBlock mfma_block(const MfmaTile& T, const MfmaArg
 __host__ __device__ inline int mfma_filter_src(const MfmaTile& T, const MfmaArgs& a,
                                                const MfmaBlock& g, int e)
 {
-    const int c_l = e / g.wch_f4;
+    const int c_l = udiv(e, g.wch_f4);
     const int e2 = e - c_l * g.wch_f4;
-    const int co_l = e2 / g.wq_f4;
+    const int co_l = udiv(e2, g.wq_f4);
     const int r4 = e2 - co_l * g.wq_f4;
     const int co = g.co0 + co_l < a.C_out - 1 ? g.co0 + co_l : a.C_out - 1;
     return c_l * g.w_cstride + (co - g.co0) * g.taps_full * T.NB + r4 * 4;
@@ -167,26 +199,26 @@ __host__ __device__ inline int mfma_slot_goff(const MfmaTile& T, const MfmaArgs&
     const int NB = T.NB, D = g.D, Do = g.Do;
     const int lrow_f4 = g.lrow_floats / 4;
     if (f < g.cc * g.slab_f4) {
-        const int c_l = f / g.slab_f4;
+        const int c_l = fdiv(f, g.fslab);
         const int fr = f - c_l * g.slab_f4;
-        const int row = fr / lrow_f4;
+        const int row = fdiv(fr, g.flrow);
         const int sr = fr - row * lrow_f4;
         const int colr = g.x0 + sr < D - 1 ? g.x0 + sr : D - 1;
-        const int col = NB == 8 ? 2 * (sr % D) + sr / D : (g.rb ? colr : sr);
+        const int col = NB == 8 ? 2 * (sr - fdiv(sr, g.fD) * D) + fdiv(sr, g.fD) : (g.rb ? colr : sr);
         int pl, yin;
         if (row < g.len0) {
             pl = g.pl0;
             yin = g.ylo0 + row;
         } else {
             const int s2 = row - g.len0;
-            pl = g.pl0 + 1 + s2 / D;
-            yin = s2 - (s2 / D) * D;
+            pl = g.pl0 + 1 + fdiv(s2, g.fD);
+            yin = s2 - fdiv(s2, g.fD) * D;
         }
         int rel;  // planes between pl0's first row and this row's plane
         if (T.KD == 2) {
             rel = (pl - g.pl0) * a.C_in;
         } else {
-            const int b = pl / Do, z = pl - (pl / Do) * Do;
+            const int b = fdiv(pl, g.fDo), z = pl - b * Do;
             rel = ((b - g.b0) * a.C_in * D + (z - g.z0));
         }
         return c_l * g.x_cstride + rel * g.plane_floats + yin * g.row_floats + col * 4;
@@ -226,7 +258,7 @@ __host__ __device__ inline int mfma_stage_channels(const MfmaTile& T, const Mfma
     int cg = s;
     qz = 0;
     if (T.KD == 3) {
-        cg = s / g.df;
+        cg = udiv(s, g.df);
         qz = s - cg * g.df;
     }
     ci0 = cg * g.cc;
@@ -309,9 +341,9 @@ __host__ __device__ inline int mfma_b_ofs(const MfmaTile& T, const MfmaBlock& g,
     const int Do = g.Do, D = g.D;
     int m = g.m0 + (l.wpos * T.NW + nw) * 16 + l.mrow;
     m = m < g.m_end - 1 ? m : g.m_end - 1;
-    const int r = m / Do;
+    const int r = fdiv(m, g.fDo);
     const int xx = m - r * Do;
-    const int pl = r / Do;
+    const int pl = fdiv(r, g.fDo);
     const int yy = r - pl * Do;
     const int srow = pl == g.pl0 ? yy - g.ylo0 : g.len0 + (pl - g.pl0 - 1) * D + yy;
     return srow * g.lrow_floats + (xx - g.x0) * 4 + l.kk;
@@ -356,7 +388,7 @@ __host__ __device__ inline int mfma_out_pos(const MfmaTile& T, const MfmaBlock& 
 __host__ __device__ inline int64_t mfma_out_ofs(const MfmaTile& T, const MfmaArgs& a, int m,
                                                 int co, int i0)
 {
-    const int b = m / a.npos;
+    const int b = udiv(m, a.npos);
     const int sp = m - b * a.npos;
     return (((int64_t)b * a.C_out + co) * a.npos + sp) * T.NB + i0;
 }

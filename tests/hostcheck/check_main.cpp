@@ -18,6 +18,7 @@
 //   conv   k g_1..g_k B C_in C_out d_image d_filter algo  ACT
 //   block  k g_1..g_k B C_in C_mid C_out d_image d_filter path  ACT ACT
 //   act    nb B C P  ACT
+//   fastdiv  (the reciprocal division of the kernels' index arithmetic)
 // with ACT = mode K blade_1..blade_K (mode -1: none, K then 0).
 // Output: one line per case, "ok <status> <launches> <simulated workgroups>
 // <kernel kinds> <tiles>" (kinds: the LaunchKind of each launch,
@@ -35,6 +36,7 @@
 
 #include "check.hpp"
 #include "cliffconv.h"
+#include "conv_mfma_geom.hpp"
 
 namespace hostcheck {
 
@@ -202,6 +204,33 @@ int main()
                                              a1.on ? &a1.d : nullptr, w2, b2,
                                              a2.on ? &a2.d : nullptr, ws, y, nullptr, path);
             }
+        } else if (kind == "fastdiv") {
+            // the kernels' division by a reciprocal (conv_mfma_geom.hpp)
+            // against integer division: every n below 2^20 for d below 64,
+            // random pairs over the whole non-negative int range, and the
+            // quotient boundaries q d - 1, q d near the top of the range
+            uint64_t rs = 0x9E3779B97F4A7C15ull;
+            auto rnd = [&]() {
+                rs ^= rs << 13;
+                rs ^= rs >> 7;
+                rs ^= rs << 17;
+                return rs;
+            };
+            auto check = [&](int n, int d) {
+                if (cliff::fdiv(n, cliff::fast_div(d)) != n / d)
+                    fail("fdiv %d / %d gives %d", n, d, cliff::fdiv(n, cliff::fast_div(d)));
+            };
+            for (int d = 1; d < 64 && !c.errors; ++d)
+                for (int n = 0; n < (1 << 20); ++n) check(n, d);
+            for (int i = 0; i < 4000000 && c.errors < 4; ++i) {
+                const int d = 1 + (int)(rnd() % (i & 1 ? 0x7FFFFFFFull : 100000ull));
+                const int n = (int)(rnd() & 0x7FFFFFFF);
+                check(n, d);
+                const int q = (0x7FFFFFFF - (int)(rnd() % 1000)) / d;
+                check(q * d, d);
+                if (q * d > 0) check(q * d - 1, d);
+            }
+            st = 0;
         } else if (kind == "act") {
             int nb;
             int64_t B, C, P;

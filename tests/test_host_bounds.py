@@ -214,6 +214,14 @@ def test_wide_112_position_tiles():
         assert int(f[5].split(".")[7]) == nw, (label, res)
 
 
+def test_reciprocal_division():
+    # the per-lane divisions of the convolution kernels' staging and fragment
+    # offsets go through a reciprocal formed once per workgroup (fdiv in
+    # conv_mfma_geom.hpp); the checker compares it with integer division
+    out = HC.run(["fastdiv"])
+    assert out == ["ok 0 0 0 - -"], out
+
+
 def act_line(nb, B, C, Pn, act):
     return "act %d %d %d %d %s" % (nb, B, C, Pn, act_field(act))
 
