@@ -87,25 +87,29 @@ class Runner:
                      for s in w.layers]
         self.g = w.layers[0].g
         self.block_path = block_path  # for entry "block2": cliff_block_path
-
-    def step(self, events=None):
-        if self.w.entry == "block2":
+        # each step's calls with their tensors checked and arguments
+        # marshalled once (the library still checks its arguments per call)
+        if w.entry == "block2":
             # one call of the two-layer block entry point; the first output
             # buffer is its workspace
+            self.plans = [P.block2_plan(self.x, self.layers[0], self.layers[1], self.g,
+                                        out=self.outs[1], workspace=self.outs[0],
+                                        path=block_path)]
+        else:
+            ins = [self.x] + self.outs[:-1]
+            self.plans = [P.conv_plan(y, f, b, self.g, act=a, out=o)
+                          for y, (f, b, a), o in zip(ins, self.layers, self.outs)]
+
+    def step(self, events=None, stream=None):
+        # events[i]: HIP events around call i, on torch's current stream (the
+        # launch stream unless `stream` is given: graph capture)
+        y = None
+        for i, plan in enumerate(self.plans):
             if events is not None:
-                events[0][0].record()
-            y = self.P.block2(self.x, self.layers[0], self.layers[1], self.g,
-                              out=self.outs[1], workspace=self.outs[0], path=self.block_path)
+                events[i][0].record()
+            y = plan(stream)
             if events is not None:
-                events[0][1].record()
-            return y
-        y = self.x
-        for li, (f, b, a) in enumerate(self.layers):
-            if events is not None:
-                events[li][0].record()
-            y = self.P.conv_nd(y, f, b, self.g, act=a, out=self.outs[li])
-            if events is not None:
-                events[li][1].record()
+                events[i][1].record()
         return y
 
     def time_graph(self, steps: int, warmup: int, per_graph: int = 1):
@@ -118,12 +122,13 @@ class Runner:
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
             for _ in range(max(1, warmup)):
-                self.step()
+                self.step(stream=side)
         torch.cuda.current_stream().wait_stream(side)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
+            cap = torch.cuda.current_stream()
             for _ in range(per_graph):
-                self.step()
+                self.step(stream=cap)
         warm(graph.replay, warmup, torch)
         replays = max(1, steps // per_graph)
         t0 = time.perf_counter()

@@ -282,15 +282,9 @@ def from_paper_protocol(filters, bias=None):
     return last(filters), last(bias)
 
 
-def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
-            out=None, stream=None, algo: int = ALGO_AUTO):
-    """Clifford convolution of GPU tensors x [B,C_in,d^k,N_B] and filters
-    [C_in,C_out,d_f^k,N_B] with bias [C_out,N_B] (or None); ``act`` is None or
-    (mode, blades, weight [C_out,K] or None, bias [C_out] or None).  Returns
-    the output tensor [B,C_out,d_out^k,N_B] (allocated with torch unless
-    ``out`` is given).  Every tensor's shape, dtype, layout and device is
-    checked before the library is called: the C ABI takes raw pointers and
-    cannot check the buffers behind them."""
+def _conv_checked(x, filters, bias, g: Sequence[int], act, out):
+    """conv_nd's checks; returns the call's sizes, the output tensor and the
+    activation descriptor."""
     import torch
     k = len(g)
     nb = 1 << k
@@ -310,7 +304,20 @@ def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
     if out is None:
         out = torch.empty(shape, dtype=torch.float32, device=x.device)
     _check_dev(out, "out", x.device)
-    desc = _act_desc(act)
+    return (k, B, C_in, C_out, d_image, d_filter), out, _act_desc(act)
+
+
+def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
+            out=None, stream=None, algo: int = ALGO_AUTO):
+    """Clifford convolution of GPU tensors x [B,C_in,d^k,N_B] and filters
+    [C_in,C_out,d_f^k,N_B] with bias [C_out,N_B] (or None); ``act`` is None or
+    (mode, blades, weight [C_out,K] or None, bias [C_out] or None).  Returns
+    the output tensor [B,C_out,d_out^k,N_B] (allocated with torch unless
+    ``out`` is given).  Every tensor's shape, dtype, layout and device is
+    checked before the library is called: the C ABI takes raw pointers and
+    cannot check the buffers behind them."""
+    (k, B, C_in, C_out, d_image, d_filter), out, desc = _conv_checked(x, filters, bias, g,
+                                                                       act, out)
     st = clifford_conv_nd_algo(k, g, B, C_in, C_out, d_image, d_filter,
                                x.data_ptr(), filters.data_ptr(),
                                bias.data_ptr() if bias is not None else 0,
@@ -318,6 +325,47 @@ def conv_nd(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
     if st != CLIFF_OK:
         raise CliffError(st, "clifford_conv_nd")
     return out
+
+
+class Plan:
+    """One library call with its tensors checked and its arguments marshalled
+    once, for callers that repeat the same call on the same buffers (loops of
+    fixed shape, benchmarks): ``plan()`` enqueues it on the stream it was made
+    for, ``plan(stream)`` on another torch stream (or raw stream handle); a
+    status other than CLIFF_OK raises CliffError.  The library checks its
+    arguments on every call as usual.  The plan holds references to its
+    tensors and descriptors; ``plan.out`` is the output tensor."""
+
+    def __init__(self, fn, args, stream_index: int, name: str, out, keep):
+        self._fn = fn
+        self._args = list(args)
+        self._si = stream_index
+        self._name = name
+        self.out = out
+        self._keep = keep
+
+    def __call__(self, stream=None):
+        if stream is not None:
+            handle = int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+            self._args[self._si] = handle or None
+        st = self._fn(*self._args)
+        if st != CLIFF_OK:
+            raise CliffError(st, self._name)
+        return self.out
+
+
+def conv_plan(x, filters, bias, g: Sequence[int], act: Optional[Tuple] = None,
+              out=None, stream=None, algo: int = ALGO_AUTO) -> Plan:
+    """conv_nd as a Plan: the checks of conv_nd once, then each call only the
+    C ABI call (``out`` is allocated here unless given)."""
+    (k, B, C_in, C_out, d_image, d_filter), out, desc = _conv_checked(x, filters, bias, g,
+                                                                       act, out)
+    garr = _g_array(g)
+    args = (k, garr, B, C_in, C_out, d_image, d_filter, x.data_ptr(), filters.data_ptr(),
+            bias.data_ptr() if bias is not None else None, out.data_ptr(),
+            ctypes.byref(desc) if desc is not None else None, _stream_ptr(stream) or None, algo)
+    return Plan(load().clifford_conv_nd_algo, args, 12, "clifford_conv_nd", out,
+                (x, filters, bias, act, garr, desc))
 
 
 def linear(x, weight, bias, g: Sequence[int], act: Optional[Tuple] = None,
@@ -395,13 +443,9 @@ def _act_desc(act):
                          ab.data_ptr() if ab is not None else 0)
 
 
-def block2(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream=None,
-           path: int = 0):
-    """Two-layer block through clifford_block2_nd: ``layer1``/``layer2`` are
-    (filters, bias or None, act or None) as in block_forward.  The workspace
-    (B * C_mid * d_mid^k * N_B floats) and the output are allocated with
-    torch unless given.  Shapes and devices are checked before the library
-    is called."""
+def _block2_checked(x, layer1, layer2, g: Sequence[int], out, workspace):
+    """block2's checks; returns the call's sizes, the workspace and output
+    tensors and both activation descriptors."""
     import torch
     k = len(g)
     nb = 1 << k
@@ -444,15 +488,46 @@ def block2(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream
         out = torch.empty(out_shape, dtype=torch.float32, device=x.device)
     _check_dev(workspace, "workspace", x.device)
     _check_dev(out, "out", x.device)
+    return ((k, B, C_in, C_mid, C_out, d_image, d_filter), workspace, out, _act_desc(a1),
+            _act_desc(a2))
+
+
+def block2(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream=None,
+           path: int = 0):
+    """Two-layer block through clifford_block2_nd: ``layer1``/``layer2`` are
+    (filters, bias or None, act or None) as in block_forward.  The workspace
+    (B * C_mid * d_mid^k * N_B floats) and the output are allocated with
+    torch unless given.  Shapes and devices are checked before the library
+    is called."""
+    (f1, b1, _), (f2, b2, _) = layer1, layer2
+    (k, B, C_in, C_mid, C_out, d_image, d_filter), workspace, out, d1, d2 = _block2_checked(
+        x, layer1, layer2, g, out, workspace)
     st = clifford_block2_nd_path(k, g, B, C_in, C_mid, C_out, d_image, d_filter,
                                  x.data_ptr(), f1.data_ptr(),
-                                 b1.data_ptr() if b1 is not None else 0, _act_desc(a1),
+                                 b1.data_ptr() if b1 is not None else 0, d1,
                                  f2.data_ptr(), b2.data_ptr() if b2 is not None else 0,
-                                 _act_desc(a2), workspace.data_ptr(), out.data_ptr(),
+                                 d2, workspace.data_ptr(), out.data_ptr(),
                                  _stream_ptr(stream), path)
     if st != CLIFF_OK:
         raise CliffError(st, "clifford_block2_nd")
     return out
+
+
+def block2_plan(x, layer1, layer2, g: Sequence[int], out=None, workspace=None, stream=None,
+                path: int = 0) -> Plan:
+    """block2 as a Plan: the checks once, then each call only the C ABI call."""
+    (f1, b1, a1), (f2, b2, a2) = layer1, layer2
+    (k, B, C_in, C_mid, C_out, d_image, d_filter), workspace, out, d1, d2 = _block2_checked(
+        x, layer1, layer2, g, out, workspace)
+    garr = _g_array(g)
+    args = (k, garr, B, C_in, C_mid, C_out, d_image, d_filter, x.data_ptr(), f1.data_ptr(),
+            b1.data_ptr() if b1 is not None else None,
+            ctypes.byref(d1) if d1 is not None else None, f2.data_ptr(),
+            b2.data_ptr() if b2 is not None else None,
+            ctypes.byref(d2) if d2 is not None else None, workspace.data_ptr(), out.data_ptr(),
+            _stream_ptr(stream) or None, path)
+    return Plan(load().clifford_block2_nd_path, args, 17, "clifford_block2_nd", out,
+                (x, layer1, layer2, workspace, garr, d1, d2))
 
 
 def block_forward(x, layers, g: Sequence[int], outs=None, stream=None):

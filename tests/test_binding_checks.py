@@ -111,3 +111,17 @@ def test_block_forward_checks_each_layer():
     x = m(2, 3, 9, 9, 4)
     layers = [(m(3, 5, 3, 3, 4), None, None), (m(4, 2, 3, 3, 4), None, None)]
     _raises(lambda: P.block_forward(x, layers[:1], G2), "x must be a GPU tensor")
+
+
+def test_plans_check_like_the_calls():
+    # a plan runs its call's checks once, at construction
+    ok = dict(x=m(*X2), filters=m(*F2), bias=m(*B2), g=G2)
+    _raises(lambda: P.conv_plan(**ok), "x must be a GPU tensor")
+    _raises(lambda: P.conv_plan(**{**ok, "bias": m(4, 4)}), "bias has shape")
+    _raises(lambda: P.conv_plan(**ok, out=m(2, 5, 7, 6, 4)), "out has shape")
+    _raises(lambda: P.conv_plan(**ok, act=(AL, (0, 1), m(4, 2), m(5))), "act weight has shape")
+    x, f1, f2 = m(2, 3, 11, 11, 4), m(3, 5, 3, 3, 4), m(5, 2, 3, 3, 4)
+    l1, l2 = (f1, m(5, 4), None), (f2, m(2, 4), None)
+    _raises(lambda: P.block2_plan(x, l1, l2, G2), "x must be a GPU tensor")
+    _raises(lambda: P.block2_plan(x, l1, (m(4, 2, 3, 3, 4), None, None), G2), "filters2 has shape")
+    _raises(lambda: P.block2_plan(x, l1, l2, G2, workspace=m(2, 5, 9, 9, 3)), "workspace holds")
