@@ -340,12 +340,15 @@ class Plan:
         self._fn = fn
         self._args = list(args)
         self._si = stream_index
+        self._stream = self._args[stream_index]
         self._name = name
         self.out = out
         self._keep = keep
 
     def __call__(self, stream=None):
-        if stream is not None:
+        if stream is None:
+            self._args[self._si] = self._stream
+        else:
             handle = int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
             self._args[self._si] = handle or None
         st = self._fn(*self._args)

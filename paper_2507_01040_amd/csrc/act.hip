@@ -112,6 +112,7 @@ cliff_status launch_act(int nb, int64_t B, int64_t C, int64_t P, const ActParams
         fprintf(stderr, "cliffconv: multivector_act N_B=%d, %lld workgroups of %d\n", nb,
                 (long long)blocks, ACT_THREADS);
     if (observe_launch(LAUNCH_ACT, {nb}, blocks, ACT_THREADS, 0, &a)) return CLIFF_OK;
+    clear_hip_error();
     switch (nb) {
     case 2: hipLaunchKernelGGL(act_kernel<2>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;
     case 4: hipLaunchKernelGGL(act_kernel<4>, dim3((unsigned)blocks), dim3(ACT_THREADS), 0, stream, a); break;

@@ -279,6 +279,7 @@ cliff_status launch_block_small(const BlockProblem& p, hipStream_t stream)
                        lds, &a))
         return CLIFF_OK;
     auto go = [&](auto kernel) {
+        clear_hip_error();
         hipLaunchKernelGGL(kernel, dim3((unsigned)n_blk), dim3(BS_THREADS), (size_t)lds, stream,
                            a);
     };

@@ -39,6 +39,11 @@ __host__ __device__ inline float sign_of(const SignMasks& s, int e)
     return ((s.neg >> e) & 1ull) ? -1.0f : 1.0f;
 }
 
+// Clears the calling thread's last HIP error before a launch, so that the
+// status read after it (hipGetLastError) is the launch's own and not that of
+// an earlier, unchecked call of the caller.
+inline void clear_hip_error() { (void)hipGetLastError(); }
+
 struct ActParams {
     int mode;     // -1: no activation
     int K;

@@ -372,6 +372,7 @@ cliff_status run1d(const ConvProblem& p, hipStream_t stream)
     if (observe_launch(LAUNCH_CONV1D_MFMA, {DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, FX, WK}, n_blk,
                        NT, lds_bytes, &a))
         return CLIFF_OK;
+    clear_hip_error();
     hipLaunchKernelGGL((conv1d_mfma_kernel<DF, WCO, WPOS, MW, NW, SIN, SW, WAVES, FW, FX, WK>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

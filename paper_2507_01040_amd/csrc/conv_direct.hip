@@ -96,6 +96,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
         fprintf(stderr, "cliffconv: conv_direct k=%d d_filter=%d, %lld workgroups of 256\n", KD,
                 (int)p.d_filter, (long long)blocks);
     if (observe_launch(LAUNCH_CONV_DIRECT, {KD, NB}, blocks, 256, 0, &a)) return CLIFF_OK;
+    clear_hip_error();
     hipLaunchKernelGGL((conv_direct_kernel<KD, NB>), dim3((unsigned)blocks), dim3(256), 0,
                        stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

@@ -571,6 +571,7 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
                        {KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, NEG}, n_blk, NT,
                        lds_bytes, &a))
         return CLIFF_OK;
+    clear_hip_error();
     hipLaunchKernelGGL((conv_mfma_kernel<KD, NB, DF, CCT, WCO, WPOS, MW, NW, SLOTS, WAVES, WK, NEG>),
                        dim3((unsigned)n_blk), dim3(NT), (size_t)lds_bytes, stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

@@ -404,6 +404,7 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
             if (observe_launch(LAUNCH_LINEAR_MFMA, {NB, RT, KQ, NWW, PF, WAVES, neg8, 512}, n_wg,
                                512, lds, &a))
                 return CLIFF_OK;
+            clear_hip_error();
             if (neg8)
                 hipLaunchKernelGGL((linear_mfma_kernel<NB, RT, KQ, NWW, PF, WAVES, true, 512>),
                                    dim3((unsigned)n_wg), dim3(512), (size_t)lds, stream, a);
@@ -416,6 +417,7 @@ cliff_status run_linear(const ConvProblem& p, hipStream_t stream)
     if (observe_launch(LAUNCH_LINEAR_MFMA, {NB, RT, KQ, NWW, PF, WAVES, neg, 256}, n_wg, 256, lds,
                        &a))
         return CLIFF_OK;
+    clear_hip_error();
     hipLaunchKernelGGL(neg ? kern_neg : kern, dim3((unsigned)n_wg), dim3(256), (size_t)lds,
                        stream, a);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;

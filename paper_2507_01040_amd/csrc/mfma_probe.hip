@@ -36,6 +36,7 @@ extern "C" cliff_status cliffconv_mfma_peak_probe(int64_t n_workgroups, int32_t 
 {
     if (!out) return CLIFF_EINVAL;
     if (n_workgroups < 1 || n_workgroups >= (1ll << 31) || iters < 1) return CLIFF_ESHAPE;
+    cliff::clear_hip_error();
     hipLaunchKernelGGL(cliff::mfma_peak_kernel, dim3((unsigned)n_workgroups), dim3(256), 0,
                        (hipStream_t)stream, (int)iters, out);
     return hipGetLastError() == hipSuccess ? CLIFF_OK : CLIFF_EDEVICE;
