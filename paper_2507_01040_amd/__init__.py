@@ -56,6 +56,11 @@ def load(path: str = LIB_PATH):
     global _lib
     if _lib is not None:
         return _lib
+    # torch first: the library then binds to the HIP runtime torch loaded (the
+    # same soname), so that streams, memory and launch errors are shared.  The
+    # other order loads a second copy of the runtime next to torch's, whose
+    # launches fail or race with torch's streams.
+    import torch  # noqa: F401
     if not os.path.exists(path):
         raise RuntimeError(
             "libcliffconv.so is not built (%s); run __graft_entry__.build()" % path)

@@ -253,3 +253,22 @@ def test_stream_algo_refuses_convolution(no_gpu):
                                  FAKE + (2 << 24), FAKE + (3 << 24), None, 0,
                                  P.ALGO_MFMA_STREAM)
     assert st == P.CLIFF_EUNSUPPORTED
+
+
+def test_one_hip_runtime_per_process():
+    # The binding loads torch before the library, so the library binds to the
+    # HIP runtime torch brought (both carry the soname libamdhip64.so.7): one
+    # runtime in the process.  Loaded the other way round, the dynamic linker
+    # maps a second copy of the runtime (torch asks for it by file name), and
+    # launches on torch's streams and memory fail or race.
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "import paper_2507_01040_amd as P\n"
+            "P.load()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n") % ROOT
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.strip().splitlines()[-1] == "1", r.stdout
