@@ -52,10 +52,6 @@ struct MfmaTile {
     }
 };
 
-// Geometry of one workgroup's block: P consecutive flattened output positions
-// [m0, m_end) (or, with row-aligned blocks, at most P positions of one output
-// row starting at column x0) by CO_WG output channels from co0, and the slab
-// of input rows it stages per channel.
 // Quotient of non-negative ints, as an unsigned division (a shorter
 // instruction sequence than the signed one); every index divided here is
 // non-negative.
@@ -83,6 +79,10 @@ __host__ __device__ inline int fdiv(int n, const FastDiv& f)
     return (int)(q * (unsigned)f.d > (unsigned)n ? q - 1 : q);
 }
 
+// Geometry of one workgroup's block: P consecutive flattened output positions
+// [m0, m_end) (or, with row-aligned blocks, at most P positions of one output
+// row starting at column x0) by CO_WG output channels from co0, and the slab
+// of input rows it stages per channel.
 struct MfmaBlock {
     int co0, m0, m_end, x0;
     int pl0, ylo0, len0, n_rows;  // slab: first plane, its first row, rows in it, total rows
