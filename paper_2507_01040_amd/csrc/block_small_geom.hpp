@@ -29,6 +29,10 @@ struct BlockArgs {
     ActParams act1, act2;
 };
 
+// Quotient of non-negative ints as an unsigned division (a shorter sequence
+// than the signed one); every index divided here is non-negative.
+__host__ __device__ inline int bs_udiv(int a, int b) { return (int)((unsigned)a / (unsigned)b); }
+
 __host__ __device__ inline int bs_ipow(int a, int k)
 {
     int r = 1;
@@ -46,7 +50,7 @@ struct BsBand {
 __host__ __device__ inline BsBand bs_band(const BlockArgs& a, int KD, int df, int bid)
 {
     BsBand g;
-    g.b = bid / a.n_band;
+    g.b = bs_udiv(bid, a.n_band);
     g.s0 = (bid - g.b * a.n_band) * a.R;
     g.R2 = a.R < a.D2 - g.s0 ? a.R : a.D2 - g.s0;
     g.R1 = g.R2 + df - 1;
@@ -64,7 +68,7 @@ __host__ __device__ inline int bs_band_f4(const BsBand& g, int NB) { return g.R0
 __host__ __device__ inline int64_t bs_band_src(const BlockArgs& a, const BsBand& g, int NB, int e)
 {
     const int ch4 = bs_band_f4(g, NB);
-    const int ci = e / ch4;
+    const int ci = bs_udiv(e, ch4);
     const int r = e - ci * ch4;
     return (((int64_t)g.b * a.C0 + ci) * a.D0 + g.s0) * g.S0 * NB + 4 * r;
 }
@@ -125,13 +129,13 @@ __host__ __device__ inline BsTile bs_tile(const BsLayer& L, int KD, int NB, int 
     const int CPT = 16 / NB;
     const int npos = L.Rout * L.Sout;
     const int RT = (L.Cout + CPT - 1) / CPT;
-    const int rt = t % RT, pt = t / RT;
+    const int pt = bs_udiv(t, RT), rt = t - pt * RT;
     BsTile T;
     T.co_r = rt * CPT + l.co_a < L.Cout - 1 ? rt * CPT + l.co_a : L.Cout - 1;
     T.m_r = pt * 16 + l.mrow < npos - 1 ? pt * 16 + l.mrow : npos - 1;
-    T.so = T.m_r / L.Sout;
+    T.so = bs_udiv(T.m_r, L.Sout);
     const int r = T.m_r - T.so * L.Sout;
-    T.yy = KD == 3 ? r / L.dout : 0;
+    T.yy = KD == 3 ? bs_udiv(r, L.dout) : 0;
     T.xx = KD == 3 ? r - T.yy * L.dout : r;
     T.a_base = T.co_r * taps * NB;
     T.b_base = (T.so * L.Sin + T.yy * L.din + T.xx) * NB + l.kk;
