@@ -12,6 +12,10 @@
 
 namespace cliff {
 
+// Quotient of non-negative ints as an unsigned division (a shorter sequence
+// than the signed one); every index divided here is non-negative.
+__host__ __device__ inline int c1_udiv(int a, int b) { return (int)((unsigned)a / (unsigned)b); }
+
 struct C1Args {
     const float* x;
     const float* w;
@@ -58,17 +62,18 @@ __host__ __device__ inline C1Block c1_block(const C1Tile& T, const C1Args& a, in
     const int Do = a.Do, D = a.D, P = T.pos();
     // XCD-aware renumbering: consecutive tiles (which share input) go to the
     // same XCD and its L2.
-    const int per = a.n_blk / 8, rem = a.n_blk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
+    const int per = a.n_blk >> 3, rem = a.n_blk & 7;
+    const int xcd = bid & 7, slot = bid >> 3;
     const int tile = xcd < rem ? xcd * (per + 1) + slot
                                : rem * (per + 1) + (xcd - rem) * per + slot;
-    const int co_blk = tile % a.n_co_blk;
-    g.m0 = (tile / a.n_co_blk) * P;
+    const int pos_blk = c1_udiv(tile, a.n_co_blk);
+    const int co_blk = tile - pos_blk * a.n_co_blk;
+    g.m0 = pos_blk * P;
     g.m_end = g.m0 + P < a.M ? g.m0 + P : a.M;
     g.co0 = co_blk * T.co_wg();
-    g.b0 = g.m0 / Do;
+    g.b0 = c1_udiv(g.m0, Do);
     g.x_first = T.FX == 4 ? (g.m0 - g.b0 * Do) & ~1 : g.m0 - g.b0 * Do;
-    g.b1 = (g.m_end - 1) / Do;
+    g.b1 = c1_udiv(g.m_end - 1, Do);
     // window length in positions: (b1 - b0) D + x_last + d_filter - x_first
     g.span = (g.b1 - g.b0) * D + (g.m_end - 1 - g.b1 * Do) + g.df - g.x_first;
     g.wch = T.co_wg() * g.df * 2;  // floats per channel of filters
@@ -85,18 +90,18 @@ __host__ __device__ inline uint32_t c1_xoffb(const C1Tile& T, const C1Args& a, c
                                              int f)
 {
     const int NB = 2, D = a.D;
-    const int c_l = f / a.span2;
+    const int c_l = c1_udiv(f, a.span2);
     const int r = f - c_l * a.span2;
     if (T.FX == 4) {
         // an even position; past the window (unused) the last even one,
         // whose pair is still inside its batch entry (d_image even)
         const int lim = (g.span - 1) & ~1;
         const int v = g.x_first + (r / NB < lim ? r / NB : lim);
-        const int bb = v / D;
+        const int bb = c1_udiv(v, D);
         return 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB);
     }
     const int v = g.x_first + (r / NB < g.span - 1 ? r / NB : g.span - 1);  // past the window: unused
-    const int bb = v / D;
+    const int bb = c1_udiv(v, D);
     return 4u * (uint32_t)((bb * a.C_in + c_l) * D * NB + (v - bb * D) * NB + (r % NB));
 }
 
@@ -109,13 +114,13 @@ __host__ __device__ inline uint32_t c1_woffb(const C1Tile& T, const C1Args& a, c
                                              int e)
 {
     const int NB = 2, df = g.df;
-    const int c_l = e / g.wch;
+    const int c_l = c1_udiv(e, g.wch);
     const int e2 = e - c_l * g.wch;
     if (T.FW == 4) {
         const int nco = T.co_wg() < a.C_out - g.co0 ? T.co_wg() : a.C_out - g.co0;
         return e2 < nco * df * NB ? 4u * (uint32_t)(c_l * a.C_out * df * NB + e2) : C1_NOLOAD;
     }
-    const int co_l = e2 / (df * NB);
+    const int co_l = c1_udiv(e2, df * NB);
     const int r = e2 - co_l * (df * NB);
     const int co = g.co0 + co_l < a.C_out - 1 ? g.co0 + co_l : a.C_out - 1;  // past C_out: unused
     return 4u * (uint32_t)(c_l * a.C_out * df * NB + (co - g.co0) * df * NB + r);
@@ -218,7 +223,7 @@ __host__ __device__ inline int c1_b_ofs(const C1Tile& T, const C1Args& a, const 
     const int Do = a.Do;
     int m = g.m0 + (l.wpos * T.NW + nw) * 16 + l.mrow;
     m = m < g.m_end - 1 ? m : g.m_end - 1;
-    const int bb = m / Do;
+    const int bb = c1_udiv(m, Do);
     return l.c_sub * a.span2 + ((bb - g.b0) * a.D + (m - bb * Do) - g.x_first) * 2 + l.j;
 }
 __host__ __device__ inline int c1_b_pair(const C1Args& a, int c_l) { return c_l * a.span2; }
@@ -247,7 +252,7 @@ __host__ __device__ inline int c1_out_channel(const C1Tile& T, const C1Block& g,
 // (c1_out_base) plus co d_out 2
 __host__ __device__ inline int64_t c1_out_base(const C1Args& a, int m)
 {
-    const int bb = m / a.Do;
+    const int bb = c1_udiv(m, a.Do);
     return ((int64_t)bb * a.C_out * a.Do + (m - bb * a.Do)) * 2;
 }
 __host__ __device__ inline int64_t c1_out_chan(const C1Args& a, int co)
