@@ -128,9 +128,12 @@ typedef enum {
                                    32 x 256 when C_out <= 32 or when a 64-
                                    channel stage does not fit) / 16 (k=3; 32
                                    when 16 < C_out <= 32 and d_filter = 3)
-                                   channels x 128 positions per workgroup
+                                   channels x 128 positions per workgroup;
+                                   k = 2 with C_out <= 16 (<= 8): 16 (8)
+                                   channels x 512 positions
                                    (on layers of >= 1 GFLOP also 96
-                                   positions for k = 2, 3, and 176 for k = 1
+                                   positions for k = 2, 3, 384 or 256 for
+                                   k = 2 with C_out <= 16, and 176 for k = 1
                                    with d_filter = 17, where those fill the
                                    last round of compute units better) */
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32

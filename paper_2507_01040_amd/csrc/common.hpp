@@ -63,6 +63,7 @@ struct ConvProblem {
     ActParams act;
     int mfma_shape;  // -1: chosen from the problem; 0..3: wide, medium, narrow, tiny
     int rowblk = 0;  // 2D row-aligned blocks: 2 where they leave <= 2 % idle (wide tiles), 1 also where whole-row slabs do not fit
+    int64_t* blocks_out = nullptr;  // set: the matrix-core tile only plans, stores its workgroup count here and launches nothing
 };
 
 // Two-layer block (conv + bias + act, twice) for the fused small-block kernel.

@@ -535,6 +535,10 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
         (rowblk && (cc + 1) * img >= (1ll << 31)) ||
         cc * p.C_out * df * df * (KD == 3 ? df : 1) * NB >= (1ll << 31))
         return CLIFF_EUNSUPPORTED;
+    if (p.blocks_out) {
+        *p.blocks_out = n_blk;
+        return CLIFF_OK;
+    }
 
     MfmaArgs a;
     a.x = p.x;
@@ -595,6 +599,23 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #define CLIFF_W3 2, 2, 4, 4, 6, 3  // same for k = 3
 #endif
 #define CLIFF_W2_32 2, 2, 4, 8, 10, 2, 1, 80 // k = 2 wide variant for C_out <= 32
+// ... and for C_out <= 16 (8) 16 (8) channels by 512, 384 or 256 positions:
+// one wave of channels, four of positions, 8, 6 or 4 MFMA tiles per wave
+#define CLIFF_W2_16 1, 4, 4, 8, 10, 2, 1, 80
+#define CLIFF_W2_16_384 1, 4, 4, 6, 10, 2, 1, 80
+#define CLIFF_W2_16_256 1, 4, 4, 4, 10, 2, 1, 80
+#define CLIFF_W2_8 1, 4, 2, 8, 10, 2, 1, 80
+#define CLIFF_W2_8_384 1, 4, 2, 6, 10, 2, 1, 80
+#define CLIFF_W2_8_256 1, 4, 2, 4, 10, 2, 1, 80
+#ifndef CLIFF_W2_16ON
+#define CLIFF_W2_16ON 1
+#endif
+#ifndef CLIFF_W2_8ON
+#define CLIFF_W2_8ON 1
+#endif
+#ifndef CLIFF_W2_SMALL_MODEL
+#define CLIFF_W2_SMALL_MODEL 1
+#endif
 // the 64-channel tile with 10 staging slots, for stages that need them
 // (large images or filters; 6 slots measured 0.4 % faster where they suffice)
 #define CLIFF_W2_S10 4, 1, 4, 8, 10, 2, 1, 80
@@ -657,15 +678,58 @@ cliff_status run_shape_cfg(const ConvProblem& p, hipStream_t stream,
 template <int KD, int NB, int DF, class Wide, class... WideAlt>
 cliff_status run_shapes(const ConvProblem& p, hipStream_t stream);
 
+// 2D, few output channels: one of three widths of the same tile (512, 384
+// or 256 positions).  On problems of >= 1 GFLOP the width whose workgroups
+// occupy the fewest position slots per CU is taken: rounds of whole blocks
+// on the CUs times the width, with the block count the kernel itself would
+// launch (row-aligned blocks with their partly idle last segment of a row
+// counted as whole blocks); ties go to the wider tile.  Otherwise, and when
+// the tile is forced, 512.
+template <int KD, int NB, int DF, class W512, class W384, class W256>
+cliff_status run_small_channels(const ConvProblem& p, hipStream_t stream)
+{
+    using Fallback = Shape<NB, CLIFF_W2_32>;
+    const int64_t M = p.B * p.d_out * p.d_out;
+    const double useful = 2.0 * M * p.C_out * NB * p.C_in * NB * (double)(p.d_filter * p.d_filter);
+    const int cus = device_cus();
+    if (CLIFF_W2_SMALL_MODEL && p.mfma_shape < 0 && useful >= 1e9 && cus > 0) {
+        constexpr int WCC = DF == 3 ? 1 : 0;
+        auto slots = [&](auto shape) -> int64_t {
+            int64_t n = 0;
+            ConvProblem q = p;
+            q.blocks_out = &n;
+            q.rowblk = 2;  // as the first attempt below: row-aligned where snug
+            if (run_shape_cfg<KD, NB, DF, WCC>(q, stream, shape) != CLIFF_OK) {
+                q.rowblk = 1;  // whole-row slabs do not fit
+                if (run_shape_cfg<KD, NB, DF, WCC>(q, stream, shape) != CLIFF_OK)
+                    return INT64_MAX;
+            }
+            return (n + cus - 1) / cus * decltype(shape)::pos;
+        };
+        const int64_t s512 = slots(W512{}), s384 = slots(W384{}), s256 = slots(W256{});
+        if (s384 < s512 && s384 <= s256) return run_shapes<KD, NB, DF, W384, Fallback>(p, stream);
+        if (s256 < s512 && s256 < s384) return run_shapes<KD, NB, DF, W256, Fallback>(p, stream);
+    }
+    return run_shapes<KD, NB, DF, W512, Fallback>(p, stream);
+}
+
 template <int KD, int NB, int DF>
 cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
 {
-    // k = 2 has two wide tiles: 64 channels x 128 positions, and for
-    // C_out <= 32 a 32 x 256 one, so the channels are not half wasted
+    // k = 2 has four wide tiles: 64 channels x 128 positions, for C_out <=
+    // 32 a 32 x 256 one, and for C_out <= 16 and <= 8 16 and 8 channels by
+    // 512 (384, 256) positions, so the channels are not half wasted
     if constexpr (KD == 2 && DF == 1) {
         if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32_LIN>>(p, stream);
         return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_LIN>>(p, stream);
     } else if constexpr (KD == 2) {
+        if (CLIFF_W2_8ON && p.C_out <= 8)
+            return run_small_channels<KD, NB, DF, Shape<NB, CLIFF_W2_8>, Shape<NB, CLIFF_W2_8_384>,
+                                      Shape<NB, CLIFF_W2_8_256>>(p, stream);
+        if (CLIFF_W2_16ON && p.C_out <= 16)
+            return run_small_channels<KD, NB, DF, Shape<NB, CLIFF_W2_16>,
+                                      Shape<NB, CLIFF_W2_16_384>, Shape<NB, CLIFF_W2_16_256>>(
+                p, stream);
         if (p.C_out <= 32) return run_shapes<KD, NB, DF, Shape<NB, CLIFF_W2_32>>(p, stream);
         // 64 channels; when their stage needs more slots (large filters or
         // images), the same tile with 10 slots, then the 32-channel tile,

@@ -214,6 +214,42 @@ def test_wide_112_position_tiles():
         assert int(f[5].split(".")[7]) == nw, (label, res)
 
 
+def test_wide_16_channel_tile():
+    # The 2D wide tile's 16-channel form (one wave of channels by four of
+    # positions, 512 positions per block), taken for C_out <= 16: the parity
+    # cases, forced and automatic, and wide images with row-aligned blocks
+    import test_parity_gpu as T
+    cases = []
+    for g, (B, C_in, C_out, d, df) in T.WIDE16_CASES:
+        for algo in (P.ALGO_MFMA_WIDE, P.ALGO_AUTO):
+            cases.append(("%s %s algo %s" % (g, (B, C_in, C_out, d, df), ALGO_NAMES[algo]),
+                          conv_line(2, g, B, C_in, C_out, d, df, algo)))
+    for B, C, d in ((2, 16, 2050), (1, 12, 4098), (128, 16, 130)):
+        cases.append(("2D B %d C %d d %d auto" % (B, C, d),
+                      conv_line(2, (1, 1), B, C, C, d, 3, P.ALGO_AUTO)))
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        f = res.split()
+        assert f[4] == "1", (label, res)  # one matrix-core launch
+        if "wide" in label or "2D B" in label or "514" in label:
+            # forced, or a problem large enough that the automatic choice
+            # takes it; the small ones may go to a narrower tile
+            assert f[5].split(".")[4:9] == ["1", "4", "4", "8", "10"], (label, res)
+
+
+def test_small_channel_tile_widths():
+    # the automatic choice among the 16- and 8-channel tiles' widths (512,
+    # 384 or 256 positions; template WCO.WPOS.MW.NW) on the GPU parity cases
+    import test_parity_gpu as T
+    cases = [("%s %s" % (g, shape), conv_line(2, g, *shape, P.ALGO_AUTO))
+             for g, shape in T.SMALL_CHANNEL_WIDTH_CASES]
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res, want in zip(cases, out, T.SMALL_CHANNEL_WIDTH_TILES):
+        f = res.split()
+        assert f[4] == "1", (label, res)
+        assert ".".join(f[5].split(".")[4:8]) == want, (label, res, want)
+
+
 def test_reciprocal_division():
     # the per-lane divisions of the convolution kernels' staging and fragment
     # offsets go through a reciprocal formed once per workgroup (fdiv in

@@ -449,6 +449,51 @@ def test_wide_112_positions(case):
     assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(case))
 
 
+# The 16-channel form of the 2D wide tile (one wave of channels, four of
+# positions, 512 positions per block) that C_out <= 16 takes: whole-row
+# slabs with a ragged last block, ragged channels, several channels per
+# stage (2x2 filter, runtime tap loop), and row-aligned blocks (d_out 512,
+# one block per row).  Forced and automatic, compared in full with the oracle.
+WIDE16_CASES = [((1, 1), (2, 16, 16, 40, 3)), ((-1, 0), (2, 7, 11, 40, 3)),
+                ((1, 1), (3, 9, 16, 35, 2)), ((1, -1), (1, 4, 16, 514, 3)),
+                ((0, 1), (1, 5, 13, 300, 3))]
+
+
+@pytest.mark.parametrize("case", WIDE16_CASES, ids=str)
+def test_wide_16_channels(case):
+    g, shape = case
+    s, x, f, b = _case(220, g, shape)
+    ref = oracle.conv_nd(x, f, b, g)
+    for algo in (P.ALGO_MFMA_WIDE, P.ALGO_AUTO):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        assert_parity(y, ref, what="%s algo %d" % (case, algo))
+
+
+# The automatic choice among the widths of the 16- and 8-channel tiles (512,
+# 384, 256 positions) on problems of >= 1 GFLOP: each case below takes the
+# width named in its comment (the host bounds test asserts which); compared in
+# full with the oracle.
+SMALL_CHANNEL_WIDTH_CASES = [
+    ((1, 1), (3, 16, 16, 258, 3)),     # 16 x 384: 512 blocks, 2 rounds
+    ((1, -1), (16, 16, 16, 66, 3)),    # 16 x 256: one round of 256 blocks
+    ((-1, 1), (1, 4, 11, 1030, 3)),    # 16 x 384, row-aligned, ragged channels
+    ((1, 1), (2, 4, 16, 300, 5)),      # 16 x 384, 5x5 filter (runtime tap loop)
+    ((1, 1), (1, 4, 8, 2050, 3)),      # 8 x 512, row-aligned (4 blocks per row)
+    ((0, -1), (2, 8, 8, 700, 3)),      # 8 x 384, row-aligned
+    ((1, 1), (64, 8, 7, 34, 3)),       # 8 x 256, ragged channels
+]
+SMALL_CHANNEL_WIDTH_TILES = ["1.4.4.6", "1.4.4.4", "1.4.4.6", "1.4.4.6", "1.4.2.8", "1.4.2.6",
+                             "1.4.2.4"]
+
+
+@pytest.mark.parametrize("case", SMALL_CHANNEL_WIDTH_CASES, ids=str)
+def test_small_channel_widths(case):
+    g, shape = case
+    s, x, f, b = _case(230, g, shape)
+    y = gpu_conv(g, x, f, b, algo=P.ALGO_AUTO)
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(case))
+
+
 # 2D, >= 1 GFLOP, 64 output channels: the automatic choice takes the wide
 # tile at 96 positions per block where its blocks fill the last round of CUs
 # better than 128 (here 737 blocks, 96 % of 3 rounds on 256 CUs, against
