@@ -128,7 +128,9 @@ typedef enum {
                                    32 x 256 when C_out <= 32 or when a 64-
                                    channel stage does not fit) / 16 (k=3; 32
                                    when 16 < C_out <= 32 and d_filter = 3)
-                                   channels x 128 positions per workgroup;
+                                   channels x 128 positions per workgroup
+                                   (k = 3, d_filter = 3, C_out <= 8: 8 x
+                                   256);
                                    k = 2 with C_out <= 16 (<= 8): 16 (8)
                                    channels x 512 positions
                                    (on layers of >= 1 GFLOP also 96

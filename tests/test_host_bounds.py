@@ -250,6 +250,25 @@ def test_small_channel_tile_widths():
         assert ".".join(f[5].split(".")[4:8]) == want, (label, res, want)
 
 
+def test_3d_8_channel_tile():
+    # the 3D 8-channel tile (template WCO.WPOS.MW.NW 1.4.4.4), forced and
+    # automatic, on the GPU parity cases and larger layers
+    import test_parity_gpu as T
+    cases = []
+    for g, shape in T.W3_8_CASES + [((1, 1, 1), (8, 8, 8, 34, 3)), ((1, 0, 1), (2, 8, 8, 66, 3))]:
+        for algo in (P.ALGO_MFMA_WIDE, P.ALGO_AUTO):
+            cases.append(("%s %s %s" % (g, shape, ALGO_NAMES[algo]),
+                          conv_line(3, g, *shape, algo)))
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        f = res.split()
+        assert f[4] == "1", (label, res)
+        if "wide" in label or ", 34, 3)" in label or ", 66, 3)" in label:
+            # forced, or large enough that the automatic choice takes it (the
+            # small layers go to the tiny tile)
+            assert ".".join(f[5].split(".")[4:8]) == "1.4.4.4", (label, res)
+
+
 def test_reciprocal_division():
     # the per-lane divisions of the convolution kernels' staging and fragment
     # offsets go through a reciprocal formed once per workgroup (fdiv in

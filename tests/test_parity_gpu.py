@@ -469,6 +469,25 @@ def test_wide_16_channels(case):
         assert_parity(y, ref, what="%s algo %d" % (case, algo))
 
 
+# The 3D 8-channel tile (3x3x3 filters, C_out <= 8: one wave of channels,
+# four of positions, 8 channels x 256 positions), forced and automatic: the
+# negated-filter form (no zero sign) and the sign-multiply form, ragged
+# channels and positions, and a >= 1 GFLOP layer; compared in full with the
+# oracle.
+W3_8_CASES = [((1, 1, 1), (2, 4, 8, 12, 3)), ((1, -1, 0), (2, 3, 7, 11, 3)),
+              ((-1, 1, 1), (1, 8, 5, 20, 3)), ((1, 1, -1), (4, 4, 8, 34, 3))]
+
+
+@pytest.mark.parametrize("case", W3_8_CASES, ids=str)
+def test_3d_8_channels(case):
+    g, shape = case
+    s, x, f, b = _case(240, g, shape)
+    ref = oracle.conv_nd(x, f, b, g)
+    for algo in (P.ALGO_MFMA_WIDE, P.ALGO_AUTO):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        assert_parity(y, ref, what="%s algo %d" % (case, algo))
+
+
 # The automatic choice among the widths of the 16- and 8-channel tiles (512,
 # 384, 256 positions) on problems of >= 1 GFLOP: each case below takes the
 # width named in its comment (the host bounds test asserts which); compared in
