@@ -269,6 +269,29 @@ def test_3d_8_channel_tile():
             assert ".".join(f[5].split(".")[4:8]) == "1.4.4.4", (label, res)
 
 
+def test_5x5_7x7_unrolled():
+    # 2D 5x5 and 7x7 filters: every matrix-core launch is the unrolled
+    # instantiation (template DF = 5, 7), on the GPU parity cases with every
+    # tile forced and on larger layers
+    import test_parity_gpu as T
+    cases = []
+    shapes = T.DF5_CASES + [((1, 1), (8, 64, 64, 128, 5)), ((1, 1), (1, 64, 64, 2052, 5)),
+                            ((1, 1), (32, 8, 8, 130, 5)), ((1, 1), (8, 64, 64, 70, 7)),
+                            ((1, 1), (2, 64, 64, 262, 7)), ((1, 1), (32, 8, 8, 134, 7))]
+    dfs = []
+    for g, shape in shapes:
+        for algo in (P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM, P.ALGO_MFMA_NARROW,
+                     P.ALGO_MFMA_TINY):
+            cases.append(("%s %s %s" % (g, shape, ALGO_NAMES[algo]),
+                          conv_line(2, g, *shape, algo)))
+            dfs.append(shape[4])
+    out = _run_cases(cases, _is_forced_tile)
+    for (label, _), res, df in zip(cases, out, dfs):
+        f = res.split()
+        if int(f[1]) == P.CLIFF_OK:
+            assert f[4] == "1" and f[5].startswith("2.4.%d." % df), (label, res)
+
+
 def test_reciprocal_division():
     # the per-lane divisions of the convolution kernels' staging and fragment
     # offsets go through a reciprocal formed once per workgroup (fdiv in

@@ -469,6 +469,29 @@ def test_wide_16_channels(case):
         assert_parity(y, ref, what="%s algo %d" % (case, algo))
 
 
+# 2D 5x5 and 7x7 filters run unrolled instantiations of every tile shape
+# (like 3x3): each shape forced and the automatic choice, ragged channels and
+# positions, a zero sign in the table, two channel blocks, and >= 1 GFLOP
+# layers; compared in full with the oracle.
+DF5_CASES = [((1, 1), (2, 8, 16, 40, 5)), ((1, -1), (1, 5, 70, 24, 5)),
+             ((1, 1), (2, 64, 64, 36, 5)), ((0, 1), (3, 3, 9, 20, 5)),
+             ((-1, -1), (2, 16, 64, 68, 5)),
+             ((1, 1), (2, 8, 16, 40, 7)), ((1, -1), (1, 5, 70, 26, 7)),
+             ((0, 1), (3, 3, 9, 20, 7)), ((1, 1), (2, 16, 64, 40, 7)),
+             ((-1, 1), (4, 8, 8, 70, 7))]
+
+
+@pytest.mark.parametrize("algo", [P.ALGO_AUTO, P.ALGO_MFMA_WIDE, P.ALGO_MFMA_MEDIUM,
+                                  P.ALGO_MFMA_NARROW, P.ALGO_MFMA_TINY],
+                         ids=["auto", "wide", "medium", "narrow", "tiny"])
+@pytest.mark.parametrize("case", DF5_CASES, ids=str)
+def test_2d_5x5_7x7_unrolled(case, algo):
+    g, shape = case
+    s, x, f, b = _case(250, g, shape)
+    y = _run_allow_unsupported(g, x, f, b, algo)
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what="%s algo %d" % (case, algo))
+
+
 # The 3D 8-channel tile (3x3x3 filters, C_out <= 8: one wave of channels,
 # four of positions, 8 channels x 256 positions), forced and automatic: the
 # negated-filter form (no zero sign) and the sign-multiply form, ragged
