@@ -124,20 +124,23 @@ typedef enum {
     CLIFF_ALGO_DIRECT = 1,      /* one thread per output multivector, fp32 FMA */
     CLIFF_ALGO_MFMA = 2,        /* implicit GEMM on fp32 MFMA, tile shape chosen
                                    from the problem size */
-    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape: 64 (k=1; k=2, or
+    CLIFF_ALGO_MFMA_WIDE = 3,   /* MFMA, forced tile shape, channels x
+                                   positions per workgroup: k = 1: 64 x 128
+                                   (d_filter = 17, layers of >= 1 GFLOP: 64
+                                   x 176 where that fills the last round of
+                                   compute units better); k = 2: 64 x 128,
                                    32 x 256 when C_out <= 32 or when a 64-
-                                   channel stage does not fit) / 16 (k=3; 32
-                                   when 16 < C_out <= 32 and d_filter = 3)
-                                   channels x 128 positions per workgroup
-                                   (k = 3, d_filter = 3, C_out <= 8: 8 x
-                                   256);
-                                   k = 2 with C_out <= 16 (<= 8): 16 (8)
-                                   channels x 512 positions
-                                   (on layers of >= 1 GFLOP also 96
-                                   positions for k = 2, 3, 384 or 256 for
-                                   k = 2 with C_out <= 16, and 176 for k = 1
-                                   with d_filter = 17, where those fill the
-                                   last round of compute units better) */
+                                   channel stage does not fit, 16 x 512
+                                   (C_out <= 16), 8 x 512 (C_out <= 8);
+                                   k = 3: 16 x 128, with d_filter = 3 32 x
+                                   128 (16 < C_out <= 32) and 8 x 256
+                                   (C_out <= 8).  The automatic choice also
+                                   takes the 96- and 112-position forms of
+                                   the 64- (k = 2) and 32-channel (k = 3)
+                                   tiles and the 384- and 256-position forms
+                                   of the 16- and 8-channel ones on layers of
+                                   >= 1 GFLOP, where they fill the last
+                                   round of compute units better */
     CLIFF_ALGO_MFMA_MEDIUM = 4, /* MFMA, 64 / 64 / 32 (k=1/2/3) channels x 32
                                    positions */
     CLIFF_ALGO_MFMA_NARROW = 5, /* MFMA, 8 / 8 / 4 channels x 256 positions */
