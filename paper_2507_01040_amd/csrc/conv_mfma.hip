@@ -641,6 +641,9 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #ifndef CLIFF_DF5
 #define CLIFF_DF5 1
 #endif
+#ifndef CLIFF_NARROW10
+#define CLIFF_NARROW10 1
+#endif
 #ifndef CLIFF_DF7
 #define CLIFF_DF7 1
 #endif
@@ -907,6 +910,11 @@ cliff_status run_shapes(const ConvProblem& p, hipStream_t stream)
             if (o == 1 && (medium_ok || forced))
                 s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Medium{});
             if (o == 2) s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Narrow{});
+            // 2D: the narrow tile with 10 staging slots, for stages that
+            // need them (large filters)
+            if constexpr (KD == 2 && CLIFF_NARROW10)
+                if (o == 2 && s == CLIFF_EUNSUPPORTED)
+                    s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Shape<NB, CLIFF_W2_8_256>{});
             if (o == 3) s = run_shape_cfg<KD, NB, DF, 0>(q, stream, Tiny{});
             if (s != CLIFF_EUNSUPPORTED) return s;
         }

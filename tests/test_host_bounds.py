@@ -292,6 +292,22 @@ def test_5x5_7x7_unrolled():
             assert f[4] == "1" and f[5].startswith("2.4.%d." % df), (label, res)
 
 
+def test_narrow_10_slots():
+    # the narrow tile's 10-slot form (template WCO.WPOS.MW.NW.SLOTS
+    # 1.4.2.4.10), taken where a large filter's stage needs more than 8 slots
+    import test_parity_gpu as T
+    cases = []
+    for g, shape in T.NARROW10_CASES + [((1, 1), (8, 64, 64, 130, 7)), ((1, 1), (2, 64, 64, 262, 7))]:
+        for algo in (P.ALGO_AUTO, P.ALGO_MFMA_NARROW):
+            cases.append(("%s %s %s" % (g, shape, ALGO_NAMES[algo]),
+                          conv_line(2, g, *shape, algo)))
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        f = res.split()
+        assert f[4] == "1", (label, res)
+        assert ".".join(f[5].split(".")[4:9]) == "1.4.2.4.10", (label, res)
+
+
 def test_reciprocal_division():
     # the per-lane divisions of the convolution kernels' staging and fragment
     # offsets go through a reciprocal formed once per workgroup (fdiv in

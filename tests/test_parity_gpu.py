@@ -492,6 +492,23 @@ def test_2d_5x5_7x7_unrolled(case, algo):
     assert_parity(y, oracle.conv_nd(x, f, b, g), what="%s algo %d" % (case, algo))
 
 
+# Large 2D filters whose stage does not fit the narrow tile's 8 staging
+# slots take its 10-slot form: 7x7 with 64 output channels, whole-row slabs
+# (d 130) and row-aligned blocks (d 262); automatic and forced narrow,
+# compared in full with the oracle.
+NARROW10_CASES = [((1, 1), (1, 8, 64, 130, 7)), ((1, -1), (1, 4, 64, 262, 7))]
+
+
+@pytest.mark.parametrize("case", NARROW10_CASES, ids=str)
+def test_narrow_10_slots(case):
+    g, shape = case
+    s, x, f, b = _case(260, g, shape)
+    ref = oracle.conv_nd(x, f, b, g)
+    for algo in (P.ALGO_AUTO, P.ALGO_MFMA_NARROW):
+        y = gpu_conv(g, x, f, b, algo=algo)
+        assert_parity(y, ref, what="%s algo %d" % (case, algo))
+
+
 # The 3D 8-channel tile (3x3x3 filters, C_out <= 8: one wave of channels,
 # four of positions, 8 channels x 256 positions), forced and automatic: the
 # negated-filter form (no zero sign) and the sign-multiply form, ragged
