@@ -625,6 +625,12 @@ cliff_status run(const ConvProblem& p, hipStream_t stream)
 #ifndef CLIFF_W2_112ON
 #define CLIFF_W2_112ON 1
 #endif
+// ... and 64 positions wide (4x4 tiles per wave), for layers too small to
+// fill the CUs with the wider blocks
+#define CLIFF_W2_64 4, 1, 4, 4, 6, 2, 1, 80
+#ifndef CLIFF_W2_64ON
+#define CLIFF_W2_64ON 1
+#endif
 // the d_filter = 1 (linear) wide kernels keep 6 slots: with 9 they spill
 #define CLIFF_W2_LIN 4, 1, 4, 8, 6, 2, 1, 80
 #define CLIFF_W2_32_LIN 2, 2, 4, 8, 6, 2, 1, 80
@@ -774,6 +780,24 @@ cliff_status run_shape(const ConvProblem& p, hipStream_t stream)
             const double f128 = fill(nblk(W128::pos, true));
             const double f112 = CLIFF_W2_112ON ? fill(nblk(W112::pos, false)) : 0.0;
             const double f96 = fill(nblk(W96::pos, false));
+            // the 64-position form (with half the MFMAs per stage it runs at
+            // about 0.85 of the wider tiles' rate when the CUs are full:
+            // measured 75.5 against 88 %) only where it still comes out
+            // ahead, and only where its 6-slot stage fits (a planning call of
+            // the kernel's own host code, no launch): else its fallbacks
+            // would be the 32-channel tile at half the blocks
+            using W64 = Shape<NB, CLIFF_W2_64>;
+            const double f64 = CLIFF_W2_64ON ? fill(nblk(W64::pos, false)) : 0.0;
+            auto fits = [&](auto shape) {
+                int64_t n = 0;
+                ConvProblem q = p;
+                q.blocks_out = &n;
+                q.rowblk = 2;
+                return run_shape_cfg<KD, NB, DF, DF == 3 ? 1 : 0>(q, stream, shape) == CLIFF_OK;
+            };
+            if (0.85 * f64 > std::max({f128, f112, f96}) && fits(W64{}))
+                return run_shapes<KD, NB, DF, W64, Shape<NB, CLIFF_W2_S10>,
+                                  Shape<NB, CLIFF_W2_32>>(p, stream);
             if (f112 > f128 && f112 >= f96)
                 return run_shapes<KD, NB, DF, W112, Shape<NB, CLIFF_W2_S10>,
                                   Shape<NB, CLIFF_W2_32>>(p, stream);

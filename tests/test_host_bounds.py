@@ -308,6 +308,20 @@ def test_narrow_10_slots():
         assert ".".join(f[5].split(".")[4:9]) == "1.4.2.4.10", (label, res)
 
 
+def test_wide_64_position_tile():
+    # the 64-position form of the 2D 64-channel wide tile (template
+    # WCO.WPOS.MW.NW 4.1.4.4), which the automatic choice takes for small
+    # single-image layers
+    import test_parity_gpu as T
+    cases = [("%s %s" % (g, shape), conv_line(2, g, *shape, P.ALGO_AUTO))
+             for g, shape in T.WIDE64_CASES + [((1, 1), (1, 64, 64, 128, 3))]]
+    out = _run_cases(cases, lambda line: False)
+    for (label, _), res in zip(cases, out):
+        f = res.split()
+        assert f[4] == "1", (label, res)
+        assert ".".join(f[5].split(".")[4:8]) == "4.1.4.4", (label, res)
+
+
 def test_reciprocal_division():
     # the per-lane divisions of the convolution kernels' staging and fragment
     # offsets go through a reciprocal formed once per workgroup (fdiv in

@@ -553,6 +553,23 @@ def test_small_channel_widths(case):
     assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(case))
 
 
+# The 64-position form of the 2D 64-channel wide tile (4x4 MFMA tiles per
+# wave), which the automatic choice takes for single-image layers of >= 1
+# GFLOP whose wider blocks would leave CUs idle (d 130 -> 128, B = 1: 256
+# blocks of 64 against 128 of 128); ragged channels, a zero sign;
+# compared in full with the oracle.
+WIDE64_CASES = [((1, 1), (1, 8, 64, 130, 3)), ((1, -1), (1, 8, 60, 130, 3)),
+                ((0, 1), (1, 8, 64, 98, 3))]
+
+
+@pytest.mark.parametrize("case", WIDE64_CASES, ids=str)
+def test_2d_wide_64_positions(case):
+    g, shape = case
+    s, x, f, b = _case(270, g, shape)
+    y = gpu_conv(g, x, f, b, algo=P.ALGO_AUTO)
+    assert_parity(y, oracle.conv_nd(x, f, b, g), what=str(case))
+
+
 # 2D, >= 1 GFLOP, 64 output channels: the automatic choice takes the wide
 # tile at 96 positions per block where its blocks fill the last round of CUs
 # better than 128 (here 737 blocks, 96 % of 3 rounds on 256 CUs, against
